@@ -1,0 +1,216 @@
+"""Throughput of one LR-QAT linear layer (forward + STE backward) on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload 2] [--no-cpu-baseline]
+
+A step is lrqat_forward followed by lrqat_backward (dX, dA, dB) on one batch of
+seeded synthetic inputs already resident in device memory: the LLaMA-7B
+q_proj-shaped layer 4096 -> 4096 with 8 x 1024 tokens, rank 32, alpha 32, W4
+per-channel and Phi0 in fixed point Q4.4 by default.  Prints one JSON line.
+
+value = algorithmic flops per step (6 T m k + 8 m k r) / step time, in TFLOP/s.
+roofline: the kernel with the largest share of the step, timed with HIP events
+on the library's stream, against the bf16 dense MFMA peak of 2.5 PFLOP/s.
+cpu_baseline: the CPU oracle on a bounded token sample of the same layer.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "LR-QAT linear fwd+bwd TFLOP/s at LLaMA-7B shapes; % of bf16 MFMA peak"
+PEAK_BF16_TFLOPS = 2500.0
+PEAK_HBM_GBS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", type=int, default=2)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU time of the oracle sample")
+    return ap.parse_args()
+
+
+def kernel_flops(name, wl, spec):
+    """Algorithmic flops of one launch of a library kernel (the useful work it does)."""
+    T, m, k, r = wl.tokens, spec.m, spec.k, wl.rank
+    return {"gemm_fwd": 2.0 * T * m * k,
+            "gemm_dx": 2.0 * T * m * k,
+            "gemm_dw": 2.0 * T * m * k + 4.0 * m * k * r,
+            "grid": 2.0 * m * k * r}.get(name)
+
+
+def traffic_record(kernel):
+    """HBM bytes per launch measured with rocprofv3 counters, if the kernel's
+    sources are unchanged since the measurement (else None)."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{kernel}.json")
+    if not os.path.exists(path):
+        return None
+    rec = json.load(open(path))
+    if rec.get("sources_sha256") != sources_sha():
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def sources_sha():
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2406_06385_amd", "csrc")
+    for f in sorted(os.listdir(csrc)):
+        h.update(f.encode())
+        h.update(open(os.path.join(csrc, f), "rb").read())
+    return h.hexdigest()
+
+
+def cpu_baseline(wl, inp, target_s):
+    """Oracle forward + backward on the first Ts tokens of the workload's layer."""
+    from oracle import lrqat_oracle as O
+    from paper_2406_06385_amd import inputs as I
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([d.get("num_threads", 1) for d in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        threads = os.cpu_count()
+    spec = wl.layers[0]
+    L = O.Layer(spec.m, spec.k, wl.rank, wl.alpha, wl.bits, wl.phi_format, wl.group_size, wl.act_bits)
+    s0 = O.minmax_scale(inp.W0, wl.bits, wl.group_size)
+    phi0 = O.encode_phi0(inp.W0, s0, wl.bits, wl.phi_format, wl.group_size)
+    X = I.bf16_bits_to_fp32(inp.X) if wl.act_dtype == "bf16" else inp.X
+    dY = (I.bf16_bits_to_fp32(inp.dY) if wl.act_dtype == "bf16" else inp.dY).astype(np.float64)
+
+    def run(ts):
+        t0 = time.perf_counter()
+        O.forward(L, X[:ts], phi0, s0, inp.A, inp.B)
+        O.backward(L, X[:ts], phi0, s0, inp.A, inp.B, dY[:ts])
+        return time.perf_counter() - t0
+
+    ts = 64
+    dt = run(ts)
+    while dt < target_s / 4 and ts < wl.tokens:
+        ts = min(wl.tokens, ts * 4)
+        dt = run(ts)
+    flops = wl.flops_fwd_bwd(ts)
+    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"float64 numpy oracle forward+backward of the same layer on its first {ts} of "
+                      f"{wl.tokens} tokens ({dt:.1f} s)"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the multi-GPU path is not part "
+              f"of this build", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    from paper_2406_06385_amd import inputs as I
+    from paper_2406_06385_amd import lrqat
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    lrqat.load_library()
+    wl = I.WORKLOADS[args.workload]
+    lspec = wl.layers[0]
+    T, m, k, r = wl.tokens, lspec.m, lspec.k, wl.rank
+    print(f"[bench] workload {wl.name}: generating inputs", file=sys.stderr, flush=True)
+    inp = I.make_layer_inputs(wl, 0)
+    spec = lrqat.LayerSpec(m, k, r, wl.alpha, wl.bits, wl.phi_format, wl.group_size, wl.act_bits, wl.act_dtype)
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    def act(a):
+        if wl.act_dtype == "bf16":
+            return torch.from_numpy(a.view(np.int16).copy()).view(torch.bfloat16).to(dev)
+        return torch.from_numpy(a).to(dev)
+
+    W0 = torch.from_numpy(inp.W0).to(dev)
+    A = torch.from_numpy(inp.A).to(dev)
+    B = torch.from_numpy(inp.B).to(dev)
+    X = act(inp.X)
+    dY = act(inp.dY)
+    s0, phi0 = lrqat.lrqat_init_from_weights(spec, W0)
+    del W0
+    Y = torch.empty((T, m), dtype=spec.torch_dtype, device=dev)
+    dX = torch.empty((T, k), dtype=spec.torch_dtype, device=dev)
+    dA = torch.empty((m, r), dtype=torch.float32, device=dev)
+    dB = torch.empty((r, k), dtype=torch.float32, device=dev)
+    ws_f = lrqat.workspace(lrqat.lrqat_forward_workspace_size(spec, T), dev)
+    ws_b = lrqat.workspace(lrqat.lrqat_backward_workspace_size(spec, T), dev)
+    stream = torch.cuda.current_stream()
+
+    def step():
+        lrqat.lrqat_forward(spec, X, phi0, s0, A, B, Y=Y, ws=ws_f, stream=stream)
+        lrqat.lrqat_backward(spec, X, phi0, s0, A, B, dY, dX=dX, dA=dA, dB=dB, ws=ws_b, stream=stream)
+
+    torch.cuda.synchronize()
+    torch.cuda.reset_peak_memory_stats(dev)
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    print(f"[bench] warmup done ({args.warmup} steps)", file=sys.stderr, flush=True)
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        step()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    ms = ev0.elapsed_time(ev1) / args.steps
+    peak_mem = torch.cuda.max_memory_allocated(dev)
+    flops = wl.flops_fwd_bwd()
+    value = flops / (ms * 1e-3) / 1e12
+    print(f"[bench] timed {args.steps} steps: {ms:.4f} ms/step", file=sys.stderr, flush=True)
+
+    # per-kernel durations (HIP events around each launch on the library's stream)
+    lrqat.lrqat_timing_reset()
+    lrqat.lrqat_timing_enable(True)
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    per = lrqat.lrqat_timing_read()
+    lrqat.lrqat_timing_enable(False)
+    lrqat.lrqat_timing_reset()
+    kernels = {n: {"launches": c, "avg_us": 1e3 * t / c} for n, (c, t) in per.items()}
+    dom = max(per, key=lambda n: per[n][1])
+    dom_avg_s = per[dom][1] / per[dom][0] * 1e-3
+    dom_flops = kernel_flops(dom, wl, lspec)
+    traffic = traffic_record(dom)
+    roofline = {"kernel": dom, "bound": "mfma", "achieved": dom_flops / dom_avg_s / 1e12 if dom_flops else None,
+                "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                "frac": (dom_flops / dom_avg_s / 1e12) / PEAK_BF16_TFLOPS if dom_flops else None,
+                "traffic": traffic}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        print("[bench] timing the CPU oracle sample", file=sys.stderr, flush=True)
+        cpu = cpu_baseline(wl, inp, args.cpu_seconds)
+
+    out = {
+        "metric": METRIC, "value": value, "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16" if wl.act_dtype == "bf16" else "fp32", "data": "synthetic",
+        "config": {"workload": wl.name, "tokens": T, "out_features": m, "in_features": k, "rank": r,
+                   "alpha": wl.alpha, "bits": wl.bits, "phi_format": wl.phi_format, "group_size": wl.group_size,
+                   "act_bits": wl.act_bits, "parallelism": "none"},
+        "pct_of_bf16_peak": 100.0 * value / PEAK_BF16_TFLOPS,
+        "tokens_per_s": T / (ms * 1e-3),
+        "peak_device_mem_bytes": int(peak_mem),
+        "kernels": kernels,
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

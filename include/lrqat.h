@@ -1,0 +1,174 @@
+/*
+ * lrqat.h -- C ABI of the LR-QAT linear layer for AMD MI355X (gfx950).
+ *
+ * LR-QAT (Bondarenko et al., "Low-Rank Quantization-Aware Training for LLMs",
+ * arXiv 2406.06385) trains a quantised linear layer through low-rank
+ * auxiliary matrices placed inside the rounding operator (Section 3,
+ * Eq. lr_qat):
+ *
+ *     W_hat = s * clip( round( Phi0 + (alpha/r) * A * B ), -2^(b-1), 2^(b-1)-1 )
+ *
+ * with W0 in R^{m x k} (m = out features, k = in features, as nn.Linear),
+ * the frozen downcast Phi0 = phi(W0 / s0) (Section 3, Eq. phi), trainable
+ * A in R^{m x r}, B in R^{r x k} and scale s.  Tokens are rows:
+ * Y = X * W_hat^T with X in R^{T x k}.  Gradients use the straight-through
+ * estimator for round() (Section 3, 'QAT with low-rank adapters') and W_hat
+ * is recomputed in the backward pass instead of being kept from the forward
+ * (Section 3, 'Gradient checkpointing').
+ *
+ * Conventions shared by every entry point
+ *   - Tensor arguments are DEVICE pointers, dense row-major, owned by the
+ *     caller; the library keeps no pointer after a call returns.
+ *   - Calls are asynchronous on `stream` (a hipStream_t; NULL = the null
+ *     stream).  Results are visible after the stream is synchronised.
+ *   - The library allocates no device memory.  Scratch space comes from the
+ *     caller as a workspace sized by the *_workspace_size queries.
+ *   - Every argument is validated on the host before any HIP call; invalid
+ *     arguments return an error status and launch nothing.  A failed launch
+ *     returns LRQAT_EHIP.  No C++ exception crosses this interface.
+ *     lrqat_last_error() gives a message for the last failure of the
+ *     calling thread.
+ *   - Calls that share a workspace must not overlap in time.
+ *   - Pointers to tensors read as 16-byte vectors must be 16-byte aligned
+ *     (X, Y, dY, dX, Phi0, W_int4, the workspace); A, B, s, dA, dB, ds and
+ *     W0 must be 4-byte aligned.
+ */
+#ifndef LRQAT_H
+#define LRQAT_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  LRQAT_OK = 0,
+  LRQAT_EINVAL = 1,        /* a null pointer, a size out of range, misalignment */
+  LRQAT_EUNSUPPORTED = 2,  /* a valid combination this library does not run */
+  LRQAT_EWORKSPACE = 3,    /* workspace smaller than the size query returns */
+  LRQAT_EHIP = 4           /* a HIP runtime or launch error */
+} lrqat_status;
+
+/* Storage format of Phi0 (Section 3, 'Downcasting operator'). */
+typedef enum {
+  /* Fixed point Qb.(8-b) in int8 (Eq. phi_fixed_point): int8 [m][k], value
+   * code / 2^(8-b).  2 <= b <= 7. */
+  LRQAT_PHI_FIXED_Q8 = 0,
+  /* INT-b, two per byte ("double-packed"): uint8 [m][k/2]; byte j of a row
+   * holds column 2j in its low nibble and column 2j+1 in its high nibble, as
+   * 4-bit two's complement.  2 <= b <= 4, k even. */
+  LRQAT_PHI_INT_PACKED2 = 1
+} lrqat_phi_format;
+
+/* Element type of the activations X, Y, dY, dX ("compute data type",
+ * Section 4.2).  A, B, s, s0, W0, dA, dB, ds are always float32. */
+typedef enum { LRQAT_FP32 = 0, LRQAT_BF16 = 1 } lrqat_dtype;
+
+typedef struct {
+  int64_t out_features;  /* m >= 1 */
+  int64_t in_features;   /* k >= 1 */
+  int32_t rank;          /* r, 1 <= r <= 256 */
+  float alpha;           /* the factor alpha of alpha/r (finite) */
+  int32_t bits;          /* b, see lrqat_phi_format; b <= 4 in this build */
+  int32_t phi_format;    /* lrqat_phi_format */
+  int64_t group_size;    /* 0: one scale per output channel, s[m];
+                            g > 0: one scale per row and group of g consecutive
+                            input columns, s[m][k/g] (Section 4, 'g128');
+                            k % g == 0 and g % 32 == 0 */
+  int32_t act_bits;      /* 0: X used as is; 8: per-token dynamic symmetric
+                            int8 fake quantisation of X with s_x[t] =
+                            max|X[t,:]|/127 and a straight-through gradient
+                            (Section 4, weight-activation quantisation);
+                            needs act_dtype = LRQAT_BF16 */
+  int32_t act_dtype;     /* lrqat_dtype */
+} lrqat_layer;
+
+/* Bytes of workspace lrqat_forward / lrqat_backward need for `tokens` rows.
+ * Returns 0 for an invalid layer (see lrqat_last_error()). */
+size_t lrqat_forward_workspace_size(const lrqat_layer* layer, int64_t tokens);
+size_t lrqat_backward_workspace_size(const lrqat_layer* layer, int64_t tokens);
+
+/*
+ * Setup: range estimation and downcast (Section 3, Eq. phi).
+ * From the pretrained weight W0 (float32 [m][k]) compute the initial scale
+ * by min-max range estimation, s0 = max|W0 over a row or row-group| /
+ * (2^(b-1)-1) (an all-zero row or group gets s0 = 1), and the frozen
+ * Phi0 = phi(W0 / s0) in `layer->phi_format`: fixed point
+ * INT8(round(2^(8-b) clip(W0/s0))) (Eq. phi_fixed_point) or double-packed
+ * INT-b clip(round(W0/s0)).  round() is half-to-even; the quotient and the
+ * rounding decision are float32.  s0_out: float32 [m] or [m][k/g];
+ * phi0_out: int8 [m][k] or uint8 [m][k/2].
+ */
+lrqat_status lrqat_init_from_weights(const lrqat_layer* layer, const float* W0,
+                                     float* s0_out, void* phi0_out, void* stream);
+
+/*
+ * Forward pass (Section 3, Eq. lr_qat): Y = X_hat * W_hat^T.
+ *   X     [T][k] act_dtype     layer input (X_hat = X, or its int8 fake
+ *                               quantisation when act_bits = 8)
+ *   phi0  Phi0 in phi_format   frozen downcast weight
+ *   s     float32 [m] or [m][k/g]
+ *   A     float32 [m][r],  B float32 [r][k]
+ *   Y     [T][m] act_dtype     output, overwritten
+ *   ws    workspace of at least lrqat_forward_workspace_size() bytes
+ * Nothing is saved for the backward pass.  T = 0 is a no-op.
+ */
+lrqat_status lrqat_forward(const lrqat_layer* layer, int64_t tokens, const void* X,
+                           const void* phi0, const float* s, const float* A, const float* B,
+                           void* Y, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Backward pass with the straight-through estimator (Section 3).  W_hat and
+ * its clip mask are recomputed from (Phi0, A, B, s); then
+ *   dX = dY * W_hat                             [T][k] act_dtype (nullable:
+ *                                               skipped when NULL)
+ *   dW = dY^T * X_hat,  G = s (.) M (.) dW       (never written to memory)
+ *   dA = (alpha/r) G B^T                        float32 [m][r]
+ *   dB = (alpha/r) A^T G                        float32 [r][k]
+ * M is the clip mask [lo <= round(Phi0 + (alpha/r) A B) <= hi].
+ * accumulate = 0 overwrites dA and dB; 1 adds into them (gradient
+ * accumulation over micro-batches).  ds (the gradient of the scale) must be
+ * NULL in this build.  With T = 0, dA and dB are zeroed (accumulate = 0) or
+ * left unchanged.  dA and dB are deterministic: the same inputs give the
+ * same bits.
+ */
+lrqat_status lrqat_backward(const lrqat_layer* layer, int64_t tokens, const void* X,
+                            const void* phi0, const float* s, const float* A, const float* B,
+                            const void* dY, void* dX, float* dA, float* dB, float* ds,
+                            int accumulate, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Merge for inference (Section 3: the adapters fuse into one b-bit integer
+ * matrix without loss): W_Z = clip(round(Phi0 + (alpha/r) A B)), written
+ * double-packed as uint8 [m][k/2] in the nibble order of
+ * LRQAT_PHI_INT_PACKED2; the inference weight is s (.) W_Z.  Needs b <= 4
+ * and k even.  No workspace.
+ */
+lrqat_status lrqat_merge_to_int4(const lrqat_layer* layer, const void* phi0, const float* A,
+                                 const float* B, uint8_t* W_int4, void* stream);
+
+/* Human-readable name of a status code (static string). */
+const char* lrqat_status_string(lrqat_status status);
+
+/* Message describing the last failed call on the calling thread ("" if none). */
+const char* lrqat_last_error(void);
+
+/*
+ * Per-kernel timing, for profiling.  When enabled, every kernel the library
+ * launches is bracketed by HIP events on its stream.  lrqat_timing_read()
+ * waits for those events and returns, for up to `max_kernels` kernel names,
+ * the name, the number of launches and their summed duration in
+ * milliseconds since the last reset; it returns the number of entries
+ * written (or -1 on a HIP error).  Names point to static strings.
+ */
+void lrqat_timing_enable(int enable);
+void lrqat_timing_reset(void);
+int lrqat_timing_read(const char** names, int64_t* launches, double* total_ms, int max_kernels);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LRQAT_H */

@@ -1,0 +1,439 @@
+// Host side of the C ABI declared in include/lrqat.h: argument validation,
+// workspace layout and the kernel sequence of each entry point.
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <map>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "kernels.h"
+#include "lrqat.h"
+
+using namespace lrqat;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+lrqat_status fail(lrqat_status st, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+lrqat_status fail(lrqat_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return st;
+}
+
+// ------------------------------------------------------------------ kernel timing
+struct Pending {
+  const char* name;
+  hipEvent_t start, stop;
+};
+std::mutex g_timing_mu;
+bool g_timing = false;
+std::vector<Pending> g_pending;
+struct Totals {
+  int64_t launches = 0;
+  double ms = 0.0;
+};
+std::map<std::string, std::pair<const char*, Totals>> g_totals;
+
+template <class F>
+hipError_t timed(const char* name, hipStream_t st, F&& launch) {
+  bool on;
+  {
+    std::lock_guard<std::mutex> lk(g_timing_mu);
+    on = g_timing;
+  }
+  if (!on) return launch();
+  hipEvent_t a, b;
+  if (hipEventCreate(&a) != hipSuccess) return hipErrorOutOfMemory;
+  if (hipEventCreate(&b) != hipSuccess) {
+    (void)hipEventDestroy(a);
+    return hipErrorOutOfMemory;
+  }
+  (void)hipEventRecord(a, st);
+  hipError_t e = launch();
+  (void)hipEventRecord(b, st);
+  std::lock_guard<std::mutex> lk(g_timing_mu);
+  g_pending.push_back({name, a, b});
+  return e;
+}
+
+// ------------------------------------------------------------------ layout
+constexpr int64_t kMaxDim = int64_t(1) << 30;
+
+inline int64_t round_up(int64_t x, int64_t a) { return (x + a - 1) / a * a; }
+inline bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
+
+struct Dims {
+  int64_t m, k, r, g, ngroups, kpad;
+  int bits, packed, act, bf16;
+  float c;
+};
+
+struct Workspace {
+  size_t q = 0, mask = 0, n = 0, sx = 0, dA_part = 0, dB_part = 0, G = 0, total = 0;
+};
+
+lrqat_status check_layer(const lrqat_layer* L, Dims& d) {
+  if (!L) return fail(LRQAT_EINVAL, "layer is NULL");
+  if (L->out_features < 1 || L->in_features < 1 || L->out_features > kMaxDim || L->in_features > kMaxDim)
+    return fail(LRQAT_EINVAL, "out_features and in_features must be in [1, 2^30] (got %lld, %lld)",
+                (long long)L->out_features, (long long)L->in_features);
+  if (L->rank < 1 || L->rank > 256) return fail(LRQAT_EINVAL, "rank must be in [1, 256] (got %d)", L->rank);
+  if (!std::isfinite(L->alpha)) return fail(LRQAT_EINVAL, "alpha must be finite");
+  if (L->phi_format != LRQAT_PHI_FIXED_Q8 && L->phi_format != LRQAT_PHI_INT_PACKED2)
+    return fail(LRQAT_EINVAL, "unknown phi_format %d", L->phi_format);
+  if (L->phi_format == LRQAT_PHI_FIXED_Q8) {
+    if (L->bits < 2 || L->bits > 7) return fail(LRQAT_EINVAL, "fixed-point Phi0 needs 2 <= bits <= 7 (got %d)", L->bits);
+    if (L->bits > 4)
+      return fail(LRQAT_EUNSUPPORTED, "bits = %d: this build keeps the integer grid as int4 and runs bits <= 4", L->bits);
+  } else {
+    if (L->bits < 2 || L->bits > 4) return fail(LRQAT_EINVAL, "packed INT-b Phi0 needs 2 <= bits <= 4 (got %d)", L->bits);
+    if (L->in_features % 2) return fail(LRQAT_EINVAL, "packed INT-b Phi0 needs an even in_features");
+  }
+  if (L->group_size < 0) return fail(LRQAT_EINVAL, "group_size must be >= 0");
+  if (L->group_size > 0) {
+    if (L->in_features % L->group_size)
+      return fail(LRQAT_EINVAL, "in_features %% group_size != 0 (%lld, %lld)", (long long)L->in_features,
+                  (long long)L->group_size);
+    if (L->group_size % 32) return fail(LRQAT_EUNSUPPORTED, "group_size must be a multiple of 32");
+  }
+  if (L->act_dtype != LRQAT_FP32 && L->act_dtype != LRQAT_BF16) return fail(LRQAT_EINVAL, "unknown act_dtype");
+  if (L->act_bits != 0 && L->act_bits != 8) return fail(LRQAT_EINVAL, "act_bits must be 0 or 8");
+  if (L->act_bits == 8 && L->act_dtype != LRQAT_BF16)
+    return fail(LRQAT_EUNSUPPORTED, "activation quantisation runs with bfloat16 activations only");
+  d.m = L->out_features;
+  d.k = L->in_features;
+  d.r = L->rank;
+  d.g = L->group_size;
+  d.ngroups = d.g ? d.k / d.g : 1;
+  d.kpad = round_up(d.k, GEMM_BN);
+  d.bits = L->bits;
+  d.packed = L->phi_format == LRQAT_PHI_INT_PACKED2;
+  d.act = L->act_bits == 8;
+  d.bf16 = L->act_dtype == LRQAT_BF16;
+  d.c = L->alpha / float(L->rank);
+  return LRQAT_OK;
+}
+
+Workspace layout(const Dims& d, int64_t T, bool backward) {
+  Workspace w;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off += size_t(round_up(int64_t(bytes), 256));
+    return at;
+  };
+  w.q = take(size_t(d.m * d.kpad / 2));
+  if (backward) w.mask = take(size_t(d.m * d.kpad / 8));
+  if (d.act) {
+    w.n = take(size_t(T * d.kpad));
+    w.sx = take(size_t(T * 4));
+  }
+  if (backward) {
+    if (d.bf16) {
+      const int64_t ntn = (d.k + GEMM_BN - 1) / GEMM_BN, ntm = (d.m + GEMM_BM - 1) / GEMM_BM;
+      w.dA_part = take(size_t(ntn * d.m * d.r * 4));
+      w.dB_part = take(size_t(2 * ntm * d.r * d.k * 4));
+    } else {
+      w.G = take(size_t(d.m * d.k * 4));
+    }
+  }
+  w.total = off;
+  return w;
+}
+
+GridArgs grid_args(const Dims& d, const void* phi0, const float* A, const float* B, uint8_t* q, uint8_t* mask) {
+  GridArgs a{};
+  a.phi0 = static_cast<const uint8_t*>(phi0);
+  a.ld_phi = d.packed ? d.k / 2 : d.k;
+  a.A = A;
+  a.B = B;
+  a.m = d.m;
+  a.k = d.k;
+  a.r = int(d.r);
+  a.c = d.c;
+  a.bits = d.bits;
+  a.packed = d.packed;
+  a.qout = q;
+  a.ldq = d.kpad / 2;
+  a.kq = d.kpad;
+  a.mout = mask;
+  a.ldm = d.kpad / 8;
+  return a;
+}
+
+lrqat_status hip_status(hipError_t e, const char* what) {
+  if (e == hipSuccess) return LRQAT_OK;
+  return fail(LRQAT_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+#define LRQAT_TRY(expr)                         \
+  do {                                          \
+    const lrqat_status st_ = (expr);            \
+    if (st_ != LRQAT_OK) return st_;            \
+  } while (0)
+
+#define NEED(ptr, align)                                                                        \
+  do {                                                                                          \
+    if (!(ptr)) return fail(LRQAT_EINVAL, "%s is NULL", #ptr);                                  \
+    if (!aligned((ptr), (align))) return fail(LRQAT_EINVAL, "%s is not %d-byte aligned", #ptr, (align)); \
+  } while (0)
+
+}  // namespace
+
+extern "C" {
+
+size_t lrqat_forward_workspace_size(const lrqat_layer* layer, int64_t tokens) {
+  Dims d;
+  if (check_layer(layer, d) != LRQAT_OK) return 0;
+  if (tokens < 0 || tokens > kMaxDim) {
+    fail(LRQAT_EINVAL, "tokens out of range");
+    return 0;
+  }
+  return layout(d, tokens, false).total;
+}
+
+size_t lrqat_backward_workspace_size(const lrqat_layer* layer, int64_t tokens) {
+  Dims d;
+  if (check_layer(layer, d) != LRQAT_OK) return 0;
+  if (tokens < 0 || tokens > kMaxDim) {
+    fail(LRQAT_EINVAL, "tokens out of range");
+    return 0;
+  }
+  return layout(d, tokens, true).total;
+}
+
+lrqat_status lrqat_init_from_weights(const lrqat_layer* layer, const float* W0, float* s0_out, void* phi0_out,
+                                     void* stream) {
+  Dims d;
+  LRQAT_TRY(check_layer(layer, d));
+  NEED(W0, 4);
+  NEED(s0_out, 4);
+  NEED(phi0_out, 16);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const int64_t gsize = d.g ? d.g : d.k;
+  LRQAT_TRY(hip_status(timed("init_scale", st, [&] { return launch_minmax_scale(W0, d.m, d.k, gsize, d.bits, s0_out, st); }),
+                       "init_scale"));
+  LRQAT_TRY(hip_status(timed("init_encode", st,
+                             [&] { return launch_encode(W0, s0_out, d.m, d.k, gsize, d.bits, d.packed, phi0_out, st); }),
+                       "init_encode"));
+  return LRQAT_OK;
+}
+
+lrqat_status lrqat_forward(const lrqat_layer* layer, int64_t tokens, const void* X, const void* phi0, const float* s,
+                           const float* A, const float* B, void* Y, void* ws, size_t ws_bytes, void* stream) {
+  Dims d;
+  LRQAT_TRY(check_layer(layer, d));
+  if (tokens < 0 || tokens > kMaxDim) return fail(LRQAT_EINVAL, "tokens out of range (%lld)", (long long)tokens);
+  if (tokens == 0) return LRQAT_OK;
+  NEED(X, 16);
+  NEED(phi0, 16);
+  NEED(s, 4);
+  NEED(A, 4);
+  NEED(B, 4);
+  NEED(Y, 16);
+  NEED(ws, 256);
+  const Workspace w = layout(d, tokens, false);
+  if (ws_bytes < w.total)
+    return fail(LRQAT_EWORKSPACE, "workspace of %zu bytes is smaller than the %zu bytes needed", ws_bytes, w.total);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  uint8_t* base = static_cast<uint8_t*>(ws);
+  uint8_t* q = base + w.q;
+  const GridArgs ga = grid_args(d, phi0, A, B, q, nullptr);
+  LRQAT_TRY(hip_status(timed("grid", st, [&] { return launch_grid(ga, st); }), "grid"));
+
+  if (!d.bf16) {
+    F32Args fa{};
+    fa.T = tokens; fa.m = d.m; fa.k = d.k; fa.r = int(d.r); fa.c = d.c;
+    fa.X = static_cast<const float*>(X);
+    fa.q = q; fa.ldq = d.kpad / 2;
+    fa.s = s; fa.gsize = d.g; fa.ngroups = d.ngroups;
+    LRQAT_TRY(hip_status(timed("f32_fwd", st, [&] { return launch_f32_forward(fa, static_cast<float*>(Y), st); }),
+                         "f32_fwd"));
+    return LRQAT_OK;
+  }
+
+  int8_t* n = reinterpret_cast<int8_t*>(base + w.n);
+  float* sx = reinterpret_cast<float*>(base + w.sx);
+  if (d.act)
+    LRQAT_TRY(hip_status(timed("act_quant", st, [&] {
+                           return launch_act_quant(static_cast<const uint16_t*>(X), tokens, d.k, n, d.kpad, sx, st);
+                         }), "act_quant"));
+  GemmArgs p{};
+  p.M = tokens; p.N = d.m; p.K = d.k;
+  p.a = d.act ? static_cast<const void*>(n) : X;
+  p.lda = d.act ? d.kpad : d.k;
+  p.b = q; p.ldb = d.kpad / 2;
+  p.s = s; p.gsize = d.g; p.ngroups = d.ngroups;
+  p.sx = d.act ? sx : nullptr;
+  p.out = Y; p.ldo = d.m;
+  LRQAT_TRY(hip_status(timed("gemm_fwd", st, [&] { return launch_gemm(kFwd, d.act, d.g != 0, p, st); }), "gemm_fwd"));
+  return LRQAT_OK;
+}
+
+lrqat_status lrqat_backward(const lrqat_layer* layer, int64_t tokens, const void* X, const void* phi0, const float* s,
+                            const float* A, const float* B, const void* dY, void* dX, float* dA, float* dB, float* ds,
+                            int accumulate, void* ws, size_t ws_bytes, void* stream) {
+  Dims d;
+  LRQAT_TRY(check_layer(layer, d));
+  if (tokens < 0 || tokens > kMaxDim) return fail(LRQAT_EINVAL, "tokens out of range (%lld)", (long long)tokens);
+  if (ds) return fail(LRQAT_EUNSUPPORTED, "the scale gradient ds is not computed by this build; pass NULL");
+  if (accumulate != 0 && accumulate != 1) return fail(LRQAT_EINVAL, "accumulate must be 0 or 1");
+  NEED(dA, 4);
+  NEED(dB, 4);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (tokens == 0) {
+    LRQAT_TRY(hip_status(launch_reduce(nullptr, 0, d.m * d.r, dA, 0.f, accumulate, st), "reduce"));
+    LRQAT_TRY(hip_status(launch_reduce(nullptr, 0, d.r * d.k, dB, 0.f, accumulate, st), "reduce"));
+    return LRQAT_OK;
+  }
+  NEED(X, 16);
+  NEED(phi0, 16);
+  NEED(s, 4);
+  NEED(A, 4);
+  NEED(B, 4);
+  NEED(dY, 16);
+  if (dX && !aligned(dX, 16)) return fail(LRQAT_EINVAL, "dX is not 16-byte aligned");
+  NEED(ws, 256);
+  const Workspace w = layout(d, tokens, true);
+  if (ws_bytes < w.total)
+    return fail(LRQAT_EWORKSPACE, "workspace of %zu bytes is smaller than the %zu bytes needed", ws_bytes, w.total);
+  uint8_t* base = static_cast<uint8_t*>(ws);
+  uint8_t* q = base + w.q;
+  uint8_t* mask = base + w.mask;
+  const GridArgs ga = grid_args(d, phi0, A, B, q, mask);
+  LRQAT_TRY(hip_status(timed("grid", st, [&] { return launch_grid(ga, st); }), "grid"));
+
+  if (!d.bf16) {
+    F32Args fa{};
+    fa.T = tokens; fa.m = d.m; fa.k = d.k; fa.r = int(d.r); fa.c = d.c;
+    fa.X = static_cast<const float*>(X);
+    fa.dY = static_cast<const float*>(dY);
+    fa.q = q; fa.ldq = d.kpad / 2;
+    fa.mask = mask; fa.ldm = d.kpad / 8;
+    fa.s = s; fa.gsize = d.g; fa.ngroups = d.ngroups;
+    fa.A = A; fa.B = B;
+    fa.G = reinterpret_cast<float*>(base + w.G);
+    if (dX)
+      LRQAT_TRY(hip_status(timed("f32_dx", st, [&] { return launch_f32_dx(fa, static_cast<float*>(dX), st); }), "f32_dx"));
+    LRQAT_TRY(hip_status(timed("f32_dw", st, [&] { return launch_f32_dw(fa, dA, dB, accumulate, st); }), "f32_dw"));
+    return LRQAT_OK;
+  }
+
+  int8_t* n = reinterpret_cast<int8_t*>(base + w.n);
+  float* sx = reinterpret_cast<float*>(base + w.sx);
+  if (d.act)
+    LRQAT_TRY(hip_status(timed("act_quant", st, [&] {
+                           return launch_act_quant(static_cast<const uint16_t*>(X), tokens, d.k, n, d.kpad, sx, st);
+                         }), "act_quant"));
+  if (dX) {
+    GemmArgs p{};
+    p.M = tokens; p.N = d.k; p.K = d.m;
+    p.a = dY; p.lda = d.m;
+    p.b = q; p.ldb = d.kpad / 2;
+    p.s = s; p.gsize = d.g; p.ngroups = d.ngroups;
+    p.out = dX; p.ldo = d.k;
+    LRQAT_TRY(hip_status(timed("gemm_dx", st, [&] { return launch_gemm(kDx, false, d.g != 0, p, st); }), "gemm_dx"));
+  }
+  float* dA_part = reinterpret_cast<float*>(base + w.dA_part);
+  float* dB_part = reinterpret_cast<float*>(base + w.dB_part);
+  GemmArgs p{};
+  p.M = d.m; p.N = d.k; p.K = tokens;
+  p.a = dY; p.lda = d.m;
+  p.b = d.act ? static_cast<const void*>(n) : X;
+  p.ldb = d.act ? d.kpad : d.k;
+  p.s = s; p.gsize = d.g; p.ngroups = d.ngroups;
+  p.sx = d.act ? sx : nullptr;
+  p.mask = mask; p.ldm = d.kpad / 8;
+  p.Am = A; p.Bm = B; p.r = int(d.r);
+  p.dA_part = dA_part; p.dB_part = dB_part;
+  LRQAT_TRY(hip_status(timed("gemm_dw", st, [&] { return launch_gemm(kDw, d.act, d.g != 0, p, st); }), "gemm_dw"));
+  const int64_t ntn = (d.k + GEMM_BN - 1) / GEMM_BN, ntm = (d.m + GEMM_BM - 1) / GEMM_BM;
+  LRQAT_TRY(hip_status(timed("reduce", st, [&] { return launch_reduce(dA_part, ntn, d.m * d.r, dA, d.c, accumulate, st); }),
+                       "reduce"));
+  LRQAT_TRY(hip_status(timed("reduce", st, [&] { return launch_reduce(dB_part, 2 * ntm, d.r * d.k, dB, d.c, accumulate, st); }),
+                       "reduce"));
+  return LRQAT_OK;
+}
+
+lrqat_status lrqat_merge_to_int4(const lrqat_layer* layer, const void* phi0, const float* A, const float* B,
+                                 uint8_t* W_int4, void* stream) {
+  Dims d;
+  LRQAT_TRY(check_layer(layer, d));
+  if (d.k % 2) return fail(LRQAT_EINVAL, "merge_to_int4 needs an even in_features");
+  NEED(phi0, 16);
+  NEED(A, 4);
+  NEED(B, 4);
+  NEED(W_int4, 16);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  GridArgs ga = grid_args(d, phi0, A, B, W_int4, nullptr);
+  ga.ldq = d.k / 2;
+  ga.kq = d.k;
+  LRQAT_TRY(hip_status(timed("merge", st, [&] { return launch_grid(ga, st); }), "merge"));
+  return LRQAT_OK;
+}
+
+const char* lrqat_status_string(lrqat_status status) {
+  switch (status) {
+    case LRQAT_OK: return "LRQAT_OK";
+    case LRQAT_EINVAL: return "LRQAT_EINVAL";
+    case LRQAT_EUNSUPPORTED: return "LRQAT_EUNSUPPORTED";
+    case LRQAT_EWORKSPACE: return "LRQAT_EWORKSPACE";
+    case LRQAT_EHIP: return "LRQAT_EHIP";
+  }
+  return "LRQAT_UNKNOWN";
+}
+
+const char* lrqat_last_error(void) { return g_last_error.c_str(); }
+
+void lrqat_timing_enable(int enable) {
+  std::lock_guard<std::mutex> lk(g_timing_mu);
+  g_timing = enable != 0;
+}
+
+void lrqat_timing_reset(void) {
+  std::lock_guard<std::mutex> lk(g_timing_mu);
+  for (auto& p : g_pending) {
+    (void)hipEventSynchronize(p.stop);
+    (void)hipEventDestroy(p.start);
+    (void)hipEventDestroy(p.stop);
+  }
+  g_pending.clear();
+  g_totals.clear();
+}
+
+int lrqat_timing_read(const char** names, int64_t* launches, double* total_ms, int max_kernels) {
+  std::lock_guard<std::mutex> lk(g_timing_mu);
+  int rc = 0;
+  for (auto& p : g_pending) {
+    float ms = 0.f;
+    if (hipEventSynchronize(p.stop) != hipSuccess || hipEventElapsedTime(&ms, p.start, p.stop) != hipSuccess) rc = -1;
+    auto& slot = g_totals[p.name];
+    slot.first = p.name;
+    slot.second.launches += 1;
+    slot.second.ms += ms;
+    (void)hipEventDestroy(p.start);
+    (void)hipEventDestroy(p.stop);
+  }
+  g_pending.clear();
+  if (rc) return rc;
+  int i = 0;
+  for (auto& kv : g_totals) {
+    if (i >= max_kernels) break;
+    if (names) names[i] = kv.second.first;
+    if (launches) launches[i] = kv.second.second.launches;
+    if (total_ms) total_ms[i] = kv.second.second.ms;
+    ++i;
+  }
+  return i;
+}
+
+}  // extern "C"

@@ -1,0 +1,487 @@
+// bf16 MFMA GEMMs of the LR-QAT layer on gfx950.
+//
+//   kFwd  Y  = X_hat W_hat^T      M = T, N = m, K = k   (Section 3, Eq. lr_qat)
+//   kDx   dX = dY W_hat           M = T, N = k, K = m
+//   kDw   dW = dY^T X_hat         M = m, N = k, K = T, never stored: the
+//         epilogue forms G = s * M * dW and the rank-r partial products
+//         G B^T and A^T G (Section 3, STE gradients w.r.t. A and B).
+//
+// W_hat enters as the packed integer grid q written by the grid pass; the
+// operand loaders unpack it into bfloat16 tiles in LDS (exact for |q| <= 8),
+// with the scale s applied in the epilogue (forward, per channel) or folded
+// into the tile (dX, and the forward with group-wise scales).
+//
+// Block tile 256 x 256 x 64, four waves in a 2 x 2 arrangement, each wave a
+// 128 x 128 sub-tile of 4 x 4 MFMA 32x32x16 blocks.  Two LDS stages of
+// (256 + 256) x 64 bfloat16 (128 KiB); the next K-tile is fetched into
+// registers while the current one feeds the MFMAs.
+#include "kernels.h"
+
+namespace lrqat {
+
+constexpr int BM = GEMM_BM, BN = GEMM_BN, BK = GEMM_BK;
+constexpr int STAGE = (BM + BN) * BK;  // bfloat16 elements per LDS stage
+
+// ------------------------------------------------------------------ K-contiguous bf16 source
+// rows x 64 tile of a row-major [rows][K] bfloat16 matrix; thread t loads
+// chunk t%8 of rows t/8 + 32 i.
+struct RegsKc {
+  u32x4 v[8];
+};
+
+__device__ __forceinline__ void load_kc_bf16(RegsKc& R, const uint16_t* __restrict__ src, int64_t ld,
+                                             int64_t row0, int64_t nrows, int64_t k0, int64_t K, bool vec) {
+  const int t = threadIdx.x;
+  const int64_t kk = k0 + 8 * (t & 7);
+  for (int i = 0; i < 8; ++i) {
+    const int64_t row = row0 + (t >> 3) + 32 * i;
+    u32x4 v = {0u, 0u, 0u, 0u};
+    if (row < nrows) {
+      const uint16_t* p = src + row * ld + kk;
+      if (vec && kk + 8 <= K) {
+        v = *reinterpret_cast<const u32x4*>(p);
+      } else {
+        uint16_t e[8];
+        for (int q = 0; q < 8; ++q) e[q] = (kk + q < K) ? p[q] : uint16_t(0);
+        for (int q = 0; q < 4; ++q) v[q] = uint32_t(e[2 * q]) | (uint32_t(e[2 * q + 1]) << 16);
+      }
+    }
+    R.v[i] = v;
+  }
+}
+
+__device__ __forceinline__ void store_kc(uint16_t* tile, const RegsKc& R) {
+  const int t = threadIdx.x;
+  for (int i = 0; i < 8; ++i) {
+    const int row = (t >> 3) + 32 * i;
+    *reinterpret_cast<u32x4*>(tile + tile_off(row, t & 7)) = R.v[i];
+  }
+}
+
+// ------------------------------------------------------------------ K-contiguous int8 source (W4A8 codes)
+struct RegsKc8 {
+  u32x2 v[8];
+};
+
+__device__ __forceinline__ void load_kc_i8(RegsKc8& R, const int8_t* __restrict__ src, int64_t ld,
+                                           int64_t row0, int64_t nrows, int64_t k0) {
+  const int t = threadIdx.x;
+  const int64_t kk = k0 + 8 * (t & 7);
+  for (int i = 0; i < 8; ++i) {
+    const int64_t row = row0 + (t >> 3) + 32 * i;
+    u32x2 v = {0u, 0u};
+    if (row < nrows) v = *reinterpret_cast<const u32x2*>(src + row * ld + kk);
+    R.v[i] = v;
+  }
+}
+
+__device__ __forceinline__ void store_kc_i8(uint16_t* tile, const RegsKc8& R) {
+  const int t = threadIdx.x;
+  for (int i = 0; i < 8; ++i) {
+    const int row = (t >> 3) + 32 * i;
+    u32x4 o;
+    for (int q = 0; q < 4; ++q) {
+      const uint32_t w = R.v[i][q >> 1];
+      o[q] = pack_bf16x2(float(sbyte(w, 2 * (q & 1))), float(sbyte(w, 2 * (q & 1) + 1)));
+    }
+    *reinterpret_cast<u32x4*>(tile + tile_off(row, t & 7)) = o;
+  }
+}
+
+// ------------------------------------------------------------------ packed q, K-contiguous (forward B)
+// 256 weight rows x 64 K-values = 256 x 32 bytes; thread t takes 16 bytes
+// (32 values) of rows t/2 and t/2 + 128.
+struct RegsQKc {
+  u32x4 v[2];
+  float sc[2];
+};
+
+template <bool GRP>
+__device__ __forceinline__ void load_q_kc(RegsQKc& R, const GemmArgs& p, int64_t row0, int64_t k0) {
+  const int t = threadIdx.x;
+  const int64_t kk = k0 + 32 * (t & 1);
+  const uint8_t* q = static_cast<const uint8_t*>(p.b);
+  for (int i = 0; i < 2; ++i) {
+    const int64_t row = row0 + (t >> 1) + 128 * i;
+    u32x4 v = {0u, 0u, 0u, 0u};
+    float sc = 0.f;
+    if (row < p.N) {
+      v = *reinterpret_cast<const u32x4*>(q + row * p.ldb + (kk >> 1));
+      if (GRP) sc = (kk < p.K) ? p.s[row * p.ngroups + kk / p.gsize] : 0.f;
+    }
+    R.v[i] = v;
+    R.sc[i] = sc;
+  }
+}
+
+template <bool GRP>
+__device__ __forceinline__ void store_q_kc(uint16_t* tile, const RegsQKc& R) {
+  const int t = threadIdx.x;
+  for (int i = 0; i < 2; ++i) {
+    const int row = (t >> 1) + 128 * i;
+    for (int c = 0; c < 4; ++c) {
+      const uint32_t w = R.v[i][c];
+      u32x4 o;
+      for (int q = 0; q < 4; ++q) {
+        float a = float(nibble(w, 2 * q)), b = float(nibble(w, 2 * q + 1));
+        if (GRP) {
+          a *= R.sc[i];
+          b *= R.sc[i];
+        }
+        o[q] = pack_bf16x2(a, b);
+      }
+      *reinterpret_cast<u32x4*>(tile + tile_off(row, 4 * (t & 1) + c)) = o;
+    }
+  }
+}
+
+// ------------------------------------------------------------------ packed q, K-strided (dX B)
+// K = weight rows (m), N = weight columns (k).  Thread t: 8 columns
+// (8 t%32 .. +7 -> 4 bytes) of 8 rows (8 (t/32) .. +7).
+struct RegsQKs {
+  uint32_t w[8];
+  float sc[8];
+};
+
+template <bool GRP>
+__device__ __forceinline__ void load_q_ks(RegsQKs& R, const GemmArgs& p, int64_t n0, int64_t k0) {
+  const int t = threadIdx.x;
+  const int64_t col = n0 + 8 * (t & 31);
+  const uint8_t* q = static_cast<const uint8_t*>(p.b);
+  for (int e = 0; e < 8; ++e) {
+    const int64_t row = k0 + 8 * (t >> 5) + e;
+    uint32_t w = 0;
+    float sc = 0.f;
+    if (row < p.K) {
+      w = *reinterpret_cast<const uint32_t*>(q + row * p.ldb + (col >> 1));
+      if (col < p.N) sc = GRP ? p.s[row * p.ngroups + col / p.gsize] : p.s[row];
+    }
+    R.w[e] = w;
+    R.sc[e] = sc;
+  }
+}
+
+__device__ __forceinline__ void store_q_ks(uint16_t* tile, const RegsQKs& R) {
+  const int t = threadIdx.x;
+  const int kg = t >> 5;
+  for (int c = 0; c < 8; ++c) {
+    u32x4 o;
+    for (int q = 0; q < 4; ++q)
+      o[q] = pack_bf16x2(float(nibble(R.w[2 * q], c)) * R.sc[2 * q],
+                         float(nibble(R.w[2 * q + 1], c)) * R.sc[2 * q + 1]);
+    *reinterpret_cast<u32x4*>(tile + tile_off(8 * (t & 31) + c, kg)) = o;
+  }
+}
+
+// ------------------------------------------------------------------ bf16, K-strided (dW A and B)
+// Tile rows = the N-like index (contiguous in memory), K = the strided index.
+// Thread t: 8 consecutive rows-of-tile (8 t%32 .. +7, one 16-byte vector) of
+// 8 K-lines (8 (t/32) .. +7); transposed in registers into 8 chunks.
+struct RegsKs {
+  u32x4 v[8];
+};
+
+__device__ __forceinline__ void load_ks_bf16(RegsKs& R, const uint16_t* __restrict__ src, int64_t ld,
+                                             int64_t c0, int64_t ncols, int64_t k0, int64_t K, bool vec) {
+  const int t = threadIdx.x;
+  const int64_t col = c0 + 8 * (t & 31);
+  for (int e = 0; e < 8; ++e) {
+    const int64_t kr = k0 + 8 * (t >> 5) + e;
+    u32x4 v = {0u, 0u, 0u, 0u};
+    if (kr < K) {
+      const uint16_t* p = src + kr * ld + col;
+      if (vec && col + 8 <= ncols) {
+        v = *reinterpret_cast<const u32x4*>(p);
+      } else {
+        uint16_t x[8];
+        for (int q = 0; q < 8; ++q) x[q] = (col + q < ncols) ? p[q] : uint16_t(0);
+        for (int q = 0; q < 4; ++q) v[q] = uint32_t(x[2 * q]) | (uint32_t(x[2 * q + 1]) << 16);
+      }
+    }
+    R.v[e] = v;
+  }
+}
+
+__device__ __forceinline__ void store_ks_bf16(uint16_t* tile, const RegsKs& R) {
+  const int t = threadIdx.x;
+  const int kg = t >> 5;
+  for (int c = 0; c < 8; ++c) {
+    u32x4 o;
+    for (int q = 0; q < 4; ++q) {
+      const uint32_t a = R.v[2 * q][c >> 1], b = R.v[2 * q + 1][c >> 1];
+      o[q] = (c & 1) ? perm_hi16(a, b) : perm_lo16(a, b);
+    }
+    *reinterpret_cast<u32x4*>(tile + tile_off(8 * (t & 31) + c, kg)) = o;
+  }
+}
+
+// int8 codes n [T][ld] times s_x[t], K-strided (dW B under W4A8).
+struct RegsKs8 {
+  u32x2 v[8];
+  float sx[8];
+};
+
+__device__ __forceinline__ void load_ks_i8(RegsKs8& R, const int8_t* __restrict__ src, int64_t ld,
+                                           const float* __restrict__ sx, int64_t c0, int64_t k0, int64_t K) {
+  const int t = threadIdx.x;
+  const int64_t col = c0 + 8 * (t & 31);
+  for (int e = 0; e < 8; ++e) {
+    const int64_t kr = k0 + 8 * (t >> 5) + e;
+    u32x2 v = {0u, 0u};
+    float s = 0.f;
+    if (kr < K) {
+      v = *reinterpret_cast<const u32x2*>(src + kr * ld + col);
+      s = sx[kr];
+    }
+    R.v[e] = v;
+    R.sx[e] = s;
+  }
+}
+
+__device__ __forceinline__ void store_ks_i8(uint16_t* tile, const RegsKs8& R) {
+  const int t = threadIdx.x;
+  const int kg = t >> 5;
+  for (int c = 0; c < 8; ++c) {
+    u32x4 o;
+    for (int q = 0; q < 4; ++q)
+      o[q] = pack_bf16x2(float(sbyte(R.v[2 * q][c >> 2], c & 3)) * R.sx[2 * q],
+                         float(sbyte(R.v[2 * q + 1][c >> 2], c & 3)) * R.sx[2 * q + 1]);
+    *reinterpret_cast<u32x4*>(tile + tile_off(8 * (t & 31) + c, kg)) = o;
+  }
+}
+
+// ------------------------------------------------------------------ the kernel
+
+template <int V, bool ACT, bool GRP>
+struct Loader;
+
+template <bool ACT, bool GRP>
+struct Loader<kFwd, ACT, GRP> {
+  typename std::conditional<ACT, RegsKc8, RegsKc>::type ra;
+  RegsQKc rb;
+  __device__ __forceinline__ void load(const GemmArgs& p, int64_t m0, int64_t n0, int64_t k0, bool vec) {
+    if constexpr (ACT) load_kc_i8(ra, static_cast<const int8_t*>(p.a), p.lda, m0, p.M, k0);
+    else load_kc_bf16(ra, static_cast<const uint16_t*>(p.a), p.lda, m0, p.M, k0, p.K, vec);
+    load_q_kc<GRP>(rb, p, n0, k0);
+  }
+  __device__ __forceinline__ void store(uint16_t* As, uint16_t* Bs) {
+    if constexpr (ACT) store_kc_i8(As, ra);
+    else store_kc(As, ra);
+    store_q_kc<GRP>(Bs, rb);
+  }
+};
+
+template <bool ACT, bool GRP>
+struct Loader<kDx, ACT, GRP> {
+  RegsKc ra;
+  RegsQKs rb;
+  __device__ __forceinline__ void load(const GemmArgs& p, int64_t m0, int64_t n0, int64_t k0, bool vec) {
+    load_kc_bf16(ra, static_cast<const uint16_t*>(p.a), p.lda, m0, p.M, k0, p.K, vec);
+    load_q_ks<GRP>(rb, p, n0, k0);
+  }
+  __device__ __forceinline__ void store(uint16_t* As, uint16_t* Bs) {
+    store_kc(As, ra);
+    store_q_ks(Bs, rb);
+  }
+};
+
+template <bool ACT, bool GRP>
+struct Loader<kDw, ACT, GRP> {
+  RegsKs ra;
+  typename std::conditional<ACT, RegsKs8, RegsKs>::type rb;
+  __device__ __forceinline__ void load(const GemmArgs& p, int64_t m0, int64_t n0, int64_t k0, bool vec) {
+    load_ks_bf16(ra, static_cast<const uint16_t*>(p.a), p.lda, m0, p.M, k0, p.K, vec);
+    if constexpr (ACT) load_ks_i8(rb, static_cast<const int8_t*>(p.b), p.ldb, p.sx, n0, k0, p.K);
+    else load_ks_bf16(rb, static_cast<const uint16_t*>(p.b), p.ldb, n0, p.N, k0, p.K, vec);
+  }
+  __device__ __forceinline__ void store(uint16_t* As, uint16_t* Bs) {
+    store_ks_bf16(As, ra);
+    if constexpr (ACT) store_ks_i8(Bs, rb);
+    else store_ks_bf16(Bs, rb);
+  }
+};
+
+// Offset of G[i][j] in the 256 x 256 bfloat16 staging tile of the dW epilogue
+// (16-byte chunks of a 512-byte row permuted by i mod 16).
+__device__ __forceinline__ int g_off(int i, int j) { return i * 256 + ((((j >> 3) ^ (i & 15))) << 3) + (j & 7); }
+
+template <int V, bool ACT, bool GRP>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void k_gemm(GemmArgs p) {
+  __shared__ __attribute__((aligned(16))) uint16_t lds[2 * STAGE];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int64_t ntm = (p.M + BM - 1) / BM;
+  const int64_t tm = blockIdx.x % ntm, tn = blockIdx.x / ntm;
+  const int64_t m0 = tm * BM, n0 = tn * BN;
+  const int wm = (wave >> 1) * 128, wn = (wave & 1) * 128;
+  // 16-byte vector loads need 8-element aligned rows
+  const bool vec = ((p.lda & 7) == 0) && (V != kDw || (p.ldb & 7) == 0);
+
+  f32x16 acc[4][4];
+  for (int a = 0; a < 4; ++a)
+    for (int b = 0; b < 4; ++b)
+      for (int v = 0; v < 16; ++v) acc[a][b][v] = 0.f;
+
+  Loader<V, ACT, GRP> ld;
+  const int nk = int((p.K + BK - 1) / BK);
+  if (nk > 0) {
+    ld.load(p, m0, n0, 0, vec);
+    ld.store(lds, lds + BM * BK);
+    __syncthreads();
+  }
+  for (int kt = 0; kt < nk; ++kt) {
+    uint16_t* As = lds + (kt & 1) * STAGE;
+    uint16_t* Bs = As + BM * BK;
+    const bool more = kt + 1 < nk;
+    if (more) ld.load(p, m0, n0, int64_t(kt + 1) * BK, vec);
+    for (int s = 0; s < 4; ++s) {
+      u32x4 af[4], bf[4];
+      const int ch = 2 * s + (lane >> 5);
+      for (int i = 0; i < 4; ++i) af[i] = *reinterpret_cast<const u32x4*>(As + tile_off(wm + 32 * i + (lane & 31), ch));
+      for (int j = 0; j < 4; ++j) bf[j] = *reinterpret_cast<const u32x4*>(Bs + tile_off(wn + 32 * j + (lane & 31), ch));
+      for (int i = 0; i < 4; ++i)
+        for (int j = 0; j < 4; ++j) acc[i][j] = mfma32(af[i], bf[j], acc[i][j]);
+    }
+    if (more) {
+      uint16_t* An = lds + ((kt + 1) & 1) * STAGE;
+      ld.store(An, An + BM * BK);
+    }
+    __syncthreads();
+  }
+
+  if constexpr (V == kFwd || V == kDx) {
+    uint16_t* out = static_cast<uint16_t*>(p.out);
+    for (int i = 0; i < 4; ++i)
+      for (int j = 0; j < 4; ++j) {
+        const int64_t col = n0 + wn + 32 * j + (lane & 31);
+        if (col >= p.N) continue;
+        float cs = 1.f;
+        if (V == kFwd && !GRP) cs = p.s[col];
+        for (int v = 0; v < 16; ++v) {
+          const int64_t row = m0 + wm + 32 * i + acc_row(v, lane);
+          if (row >= p.M) continue;
+          float val = acc[i][j][v] * cs;
+          if (V == kFwd && ACT) val *= p.sx[row];
+          out[row * p.ldo + col] = __builtin_bit_cast(uint16_t, (__bf16)val);
+        }
+      }
+  } else {
+    // ---- G = s * M * dW, kept in registers (fp32) and staged in LDS (bf16)
+    uint16_t* Gs = lds;
+    for (int i = 0; i < 4; ++i)
+      for (int j = 0; j < 4; ++j) {
+        const int lj = wn + 32 * j + (lane & 31);
+        const int64_t col = n0 + lj;
+        for (int v = 0; v < 16; ++v) {
+          const int li = wm + 32 * i + acc_row(v, lane);
+          const int64_t row = m0 + li;
+          float g = 0.f;
+          if (row < p.M && col < p.N) {
+            const float sc = GRP ? p.s[row * p.ngroups + col / p.gsize] : p.s[row];
+            const int bit = (p.mask[row * p.ldm + (col >> 3)] >> (col & 7)) & 1;
+            g = bit ? acc[i][j][v] * sc : 0.f;
+          }
+          acc[i][j][v] = g;
+          Gs[g_off(li, lj)] = __builtin_bit_cast(uint16_t, (__bf16)g);
+        }
+      }
+    __syncthreads();
+
+    const int r = p.r;
+    const int nrb = (r + 31) / 32;
+    const int half = lane >> 5;
+    // ---- dA partial [tn][row][rho] = sum_j G[row][j] B[rho][n0 + j]   (A operand from LDS)
+    for (int pr = wave; pr < 8 * nrb; pr += 4) {
+      const int rowblk = pr & 7, rb = pr >> 3;
+      const int rho = 32 * rb + (lane & 31);
+      f32x16 d;
+      for (int v = 0; v < 16; ++v) d[v] = 0.f;
+      for (int s = 0; s < 16; ++s) {
+        const int li = 32 * rowblk + (lane & 31);
+        const u32x4 aop = *reinterpret_cast<const u32x4*>(Gs + g_off(li, 16 * s + 8 * half));
+        float x[8];
+        const int64_t jb = n0 + 16 * s + 8 * half;
+        for (int e = 0; e < 8; ++e) x[e] = (rho < r && jb + e < p.N) ? p.Bm[int64_t(rho) * p.N + jb + e] : 0.f;
+        u32x4 bop;
+        for (int q = 0; q < 4; ++q) bop[q] = pack_bf16x2(x[2 * q], x[2 * q + 1]);
+        d = mfma32(aop, bop, d);
+      }
+      if (rho < r) {
+        for (int v = 0; v < 16; ++v) {
+          const int64_t row = m0 + 32 * rowblk + acc_row(v, lane);
+          if (row < p.M) p.dA_part[(tn * p.M + row) * r + rho] = d[v];
+        }
+      }
+    }
+    // ---- dB partial [2 tm + wave row][rho][col] = sum_i A[m0 + i][rho] G[i][col]  (G from registers)
+    const int64_t part = 2 * tm + (wave >> 1);
+    for (int rb = 0; rb < nrb; ++rb) {
+      const int rho = 32 * rb + (lane & 31);
+      u32x4 aop[4][2];
+      for (int i = 0; i < 4; ++i)
+        for (int s = 0; s < 2; ++s) {
+          float x[8];
+          for (int e = 0; e < 8; ++e) {
+            const int64_t row = m0 + wm + 32 * i + acc_row(8 * s + e, lane);
+            x[e] = (rho < r && row < p.M) ? p.Am[row * r + rho] : 0.f;
+          }
+          for (int q = 0; q < 4; ++q) aop[i][s][q] = pack_bf16x2(x[2 * q], x[2 * q + 1]);
+        }
+      for (int j = 0; j < 4; ++j) {
+        f32x16 d;
+        for (int v = 0; v < 16; ++v) d[v] = 0.f;
+        for (int i = 0; i < 4; ++i)
+          for (int s = 0; s < 2; ++s) {
+            u32x4 gop;
+            for (int q = 0; q < 4; ++q) gop[q] = pack_bf16x2(acc[i][j][8 * s + 2 * q], acc[i][j][8 * s + 2 * q + 1]);
+            d = mfma32(aop[i][s], gop, d);
+          }
+        const int64_t col = n0 + wn + 32 * j + (lane & 31);
+        if (col < p.N) {
+          for (int v = 0; v < 16; ++v) {
+            const int rr = 32 * rb + acc_row(v, lane);
+            if (rr < r) p.dB_part[(part * r + rr) * p.N + col] = d[v];
+          }
+        }
+      }
+    }
+  }
+}
+
+// Deterministic sum of partial buffers: out = (accumulate ? out : 0) + c * sum_p part[p].
+__global__ __launch_bounds__(256) void k_reduce(const float* __restrict__ part, int64_t nparts, int64_t n,
+                                                float* __restrict__ out, float c, int accumulate) {
+  const int64_t idx = int64_t(blockIdx.x) * 256 + threadIdx.x;
+  if (idx >= n) return;
+  float s = 0.f;
+  for (int64_t q = 0; q < nparts; ++q) s += part[q * n + idx];
+  out[idx] = (accumulate ? out[idx] : 0.f) + c * s;
+}
+
+template <int V, bool ACT, bool GRP>
+static hipError_t launch_variant(const GemmArgs& p, hipStream_t st) {
+  const int64_t ntm = (p.M + BM - 1) / BM, ntn = (p.N + BN - 1) / BN;
+  k_gemm<V, ACT, GRP><<<unsigned(ntm * ntn), 256, 0, st>>>(p);
+  return hipGetLastError();
+}
+
+hipError_t launch_gemm(GemmVariant v, bool act, bool grouped, const GemmArgs& p, hipStream_t st) {
+  switch (v) {
+    case kFwd:
+      if (act) return grouped ? launch_variant<kFwd, true, true>(p, st) : launch_variant<kFwd, true, false>(p, st);
+      return grouped ? launch_variant<kFwd, false, true>(p, st) : launch_variant<kFwd, false, false>(p, st);
+    case kDx:
+      return grouped ? launch_variant<kDx, false, true>(p, st) : launch_variant<kDx, false, false>(p, st);
+    case kDw:
+      if (act) return grouped ? launch_variant<kDw, true, true>(p, st) : launch_variant<kDw, true, false>(p, st);
+      return grouped ? launch_variant<kDw, false, true>(p, st) : launch_variant<kDw, false, false>(p, st);
+  }
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_reduce(const float* part, int64_t nparts, int64_t n, float* out, float c, int accumulate,
+                         hipStream_t st) {
+  k_reduce<<<unsigned((n + 255) / 256), 256, 0, st>>>(part, nparts, n, out, c, accumulate);
+  return hipGetLastError();
+}
+
+}  // namespace lrqat

@@ -1,0 +1,84 @@
+// Kernel argument blocks and host-side launchers of the LR-QAT library.
+#pragma once
+
+#include "common.h"
+
+namespace lrqat {
+
+// Integer grid pass (reconstruction / merge).
+struct GridArgs {
+  const uint8_t* phi0;   // Phi0: int8 [m][ld_phi] (fixed point) or uint8 [m][ld_phi] packed
+  int64_t ld_phi;        // bytes per row of phi0
+  const float* A;        // [m][r]
+  const float* B;        // [r][k]
+  int64_t m, k;
+  int r;
+  float c;               // alpha / r
+  int bits;
+  int packed;            // 1: Phi0 is double-packed INT-b
+  uint8_t* qout;         // packed q [m][ldq]
+  int64_t ldq;           // bytes per row of qout
+  int64_t kq;            // columns written per row of qout (>= k; columns >= k are 0)
+  uint8_t* mout;         // clip-mask bits [m][ldm] (nullable)
+  int64_t ldm;           // bytes per row of mout
+};
+
+// bf16 MFMA GEMM family.  C[M][N] = sum_K a(M, K) b(K, N) with the operand
+// sources and epilogue chosen by the kernel variant.
+enum GemmVariant { kFwd = 0, kDx = 1, kDw = 2 };
+
+struct GemmArgs {
+  int64_t M, N, K;
+  const void* a;          // kFwd: X bf16 [T][k] or n int8 [T][lda]; kDx: dY [T][m]; kDw: dY [T][m]
+  int64_t lda;
+  const void* b;          // kFwd/kDx: packed q [m][ldb]; kDw: X bf16 [T][k] or n int8 [T][ldb]
+  int64_t ldb;
+  const float* s;         // weight scale [m] or [m][ngroups]
+  int64_t gsize, ngroups;
+  const float* sx;        // per-token activation scale [T] (W4A8) or null
+  void* out;              // kFwd: Y [T][m]; kDx: dX [T][k]
+  int64_t ldo;
+  const uint8_t* mask;    // kDw: clip-mask bits [m][ldm]
+  int64_t ldm;
+  const float* Am;        // kDw: A [m][r]
+  const float* Bm;        // kDw: B [r][k]
+  int r;
+  float* dA_part;         // kDw: [ceil(N/256)][M][r]
+  float* dB_part;         // kDw: [2*ceil(M/256)][r][N]
+};
+
+constexpr int GEMM_BM = 256, GEMM_BN = 256, GEMM_BK = 64;
+
+hipError_t launch_minmax_scale(const float* W0, int64_t m, int64_t k, int64_t gsize, int bits, float* s0,
+                               hipStream_t st);
+hipError_t launch_encode(const float* W0, const float* s0, int64_t m, int64_t k, int64_t gsize, int bits,
+                         int packed, void* phi0, hipStream_t st);
+hipError_t launch_grid(const GridArgs& a, hipStream_t st);
+hipError_t launch_act_quant(const uint16_t* X, int64_t T, int64_t k, int8_t* n, int64_t ldn, float* sx,
+                            hipStream_t st);
+hipError_t launch_gemm(GemmVariant v, bool act, bool grouped, const GemmArgs& p, hipStream_t st);
+hipError_t launch_reduce(const float* part, int64_t nparts, int64_t n, float* out, float c, int accumulate,
+                         hipStream_t st);
+
+// float32 activation path (simple tiled FMA kernels).
+struct F32Args {
+  int64_t T, m, k;
+  int r;
+  float c;
+  const float* X;
+  const float* dY;
+  const uint8_t* q;       // packed q [m][ldq]
+  int64_t ldq;
+  const uint8_t* mask;    // [m][ldm]
+  int64_t ldm;
+  const float* s;
+  int64_t gsize, ngroups;
+  const float* A;
+  const float* B;
+  float* G;               // workspace [m][k]
+};
+hipError_t launch_f32_forward(const F32Args& a, float* Y, hipStream_t st);
+hipError_t launch_f32_dx(const F32Args& a, float* dX, hipStream_t st);
+hipError_t launch_f32_dw(const F32Args& a, float* dA, float* dB, int accumulate, hipStream_t st);
+
+}  // namespace lrqat

@@ -1,0 +1,224 @@
+"""Python binding of the LR-QAT C ABI (include/lrqat.h).
+
+Argument marshalling only: every step of the layer runs in the HIP library
+liblrqat.so.  torch provides device memory (tensors) and the current stream.
+The functions keep the C names; tensors must be contiguous and on the GPU.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "liblrqat.so")
+
+LRQAT_OK, LRQAT_EINVAL, LRQAT_EUNSUPPORTED, LRQAT_EWORKSPACE, LRQAT_EHIP = range(5)
+PHI_FIXED_Q8, PHI_INT_PACKED2 = 0, 1
+FP32, BF16 = 0, 1
+_FMT = {"q8": PHI_FIXED_Q8, "int_packed2": PHI_INT_PACKED2}
+_DT = {"fp32": FP32, "bf16": BF16}
+
+
+class _Layer(ctypes.Structure):
+    _fields_ = [("out_features", ctypes.c_int64), ("in_features", ctypes.c_int64),
+                ("rank", ctypes.c_int32), ("alpha", ctypes.c_float), ("bits", ctypes.c_int32),
+                ("phi_format", ctypes.c_int32), ("group_size", ctypes.c_int64),
+                ("act_bits", ctypes.c_int32), ("act_dtype", ctypes.c_int32)]
+
+
+@dataclass(frozen=True)
+class LayerSpec:
+    """Hyper-parameters of one LR-QAT linear (mirrors the C struct lrqat_layer)."""
+    out_features: int
+    in_features: int
+    rank: int
+    alpha: float
+    bits: int
+    phi_format: str = "q8"        # "q8" or "int_packed2"
+    group_size: int = 0
+    act_bits: int = 0
+    act_dtype: str = "bf16"       # "bf16" or "fp32"
+
+    def c_struct(self) -> _Layer:
+        return _Layer(self.out_features, self.in_features, self.rank, self.alpha, self.bits,
+                      _FMT[self.phi_format], self.group_size, self.act_bits, _DT[self.act_dtype])
+
+    @property
+    def torch_dtype(self):
+        return torch.bfloat16 if self.act_dtype == "bf16" else torch.float32
+
+    def scale_shape(self):
+        m, k, g = self.out_features, self.in_features, self.group_size
+        return (m,) if g == 0 else (m, k // g)
+
+    def phi_shape(self):
+        m, k = self.out_features, self.in_features
+        return (m, k) if self.phi_format == "q8" else (m, k // 2)
+
+    @property
+    def phi_dtype(self):
+        return torch.int8 if self.phi_format == "q8" else torch.uint8
+
+
+class LRQATError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{_lib().lrqat_status_string(status).decode()}: {message}")
+        self.status = status
+
+
+_LIB = None
+
+
+def _lib():
+    global _LIB
+    if _LIB is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is not built; run `python -m paper_2406_06385_amd.build`")
+        lib = ctypes.CDLL(LIB_PATH)
+        P, I64, SZ, F = ctypes.c_void_p, ctypes.c_int64, ctypes.c_size_t, ctypes.POINTER(_Layer)
+        lib.lrqat_forward_workspace_size.argtypes = [F, I64]
+        lib.lrqat_forward_workspace_size.restype = SZ
+        lib.lrqat_backward_workspace_size.argtypes = [F, I64]
+        lib.lrqat_backward_workspace_size.restype = SZ
+        lib.lrqat_init_from_weights.argtypes = [F, P, P, P, P]
+        lib.lrqat_forward.argtypes = [F, I64, P, P, P, P, P, P, P, SZ, P]
+        lib.lrqat_backward.argtypes = [F, I64, P, P, P, P, P, P, P, P, P, P, ctypes.c_int, P, SZ, P]
+        lib.lrqat_merge_to_int4.argtypes = [F, P, P, P, P, P]
+        for fn in ("lrqat_init_from_weights", "lrqat_forward", "lrqat_backward", "lrqat_merge_to_int4"):
+            getattr(lib, fn).restype = ctypes.c_int
+        lib.lrqat_status_string.argtypes = [ctypes.c_int]
+        lib.lrqat_status_string.restype = ctypes.c_char_p
+        lib.lrqat_last_error.restype = ctypes.c_char_p
+        lib.lrqat_timing_enable.argtypes = [ctypes.c_int]
+        lib.lrqat_timing_read.argtypes = [ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(I64),
+                                          ctypes.POINTER(ctypes.c_double), ctypes.c_int]
+        lib.lrqat_timing_read.restype = ctypes.c_int
+        _LIB = lib
+    return _LIB
+
+
+def load_library() -> str:
+    """Load liblrqat.so (raises if it is missing) and return its path."""
+    _lib()
+    return LIB_PATH
+
+
+def _check(status: int):
+    if status != LRQAT_OK:
+        raise LRQATError(status, _lib().lrqat_last_error().decode())
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    if not isinstance(t, torch.Tensor):
+        raise TypeError("expected a torch.Tensor")
+    if not t.is_cuda or not t.is_contiguous():
+        raise ValueError("tensors passed to the LR-QAT library must be contiguous GPU tensors")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _expect(t, shape, dtype, name):
+    if tuple(t.shape) != tuple(shape) or t.dtype != dtype:
+        raise ValueError(f"{name}: expected {tuple(shape)} {dtype}, got {tuple(t.shape)} {t.dtype}")
+
+
+def lrqat_forward_workspace_size(spec: LayerSpec, tokens: int) -> int:
+    L = spec.c_struct()
+    n = _lib().lrqat_forward_workspace_size(ctypes.byref(L), tokens)
+    if n == 0:
+        raise LRQATError(LRQAT_EINVAL, _lib().lrqat_last_error().decode())
+    return n
+
+
+def lrqat_backward_workspace_size(spec: LayerSpec, tokens: int) -> int:
+    L = spec.c_struct()
+    n = _lib().lrqat_backward_workspace_size(ctypes.byref(L), tokens)
+    if n == 0:
+        raise LRQATError(LRQAT_EINVAL, _lib().lrqat_last_error().decode())
+    return n
+
+
+def workspace(nbytes: int, device="cuda") -> torch.Tensor:
+    return torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=device)
+
+
+def lrqat_init_from_weights(spec: LayerSpec, W0: torch.Tensor, stream=None):
+    """-> (s0 float32, Phi0) computed on the GPU from W0 [m][k] float32."""
+    _expect(W0, (spec.out_features, spec.in_features), torch.float32, "W0")
+    s0 = torch.empty(spec.scale_shape(), dtype=torch.float32, device=W0.device)
+    phi0 = torch.empty(spec.phi_shape(), dtype=spec.phi_dtype, device=W0.device)
+    L = spec.c_struct()
+    _check(_lib().lrqat_init_from_weights(ctypes.byref(L), _ptr(W0), _ptr(s0), _ptr(phi0), _stream(stream)))
+    return s0, phi0
+
+
+def lrqat_forward(spec: LayerSpec, X, phi0, s, A, B, Y=None, ws=None, stream=None):
+    """Y = X_hat W_hat^T.  X [T][k] in the layer's activation dtype."""
+    T = X.shape[0]
+    _expect(X, (T, spec.in_features), spec.torch_dtype, "X")
+    if Y is None:
+        Y = torch.empty((T, spec.out_features), dtype=spec.torch_dtype, device=X.device)
+    if ws is None:
+        ws = workspace(lrqat_forward_workspace_size(spec, T), X.device)
+    L = spec.c_struct()
+    _check(_lib().lrqat_forward(ctypes.byref(L), T, _ptr(X), _ptr(phi0), _ptr(s), _ptr(A), _ptr(B), _ptr(Y),
+                                _ptr(ws), ws.numel(), _stream(stream)))
+    return Y
+
+
+def lrqat_backward(spec: LayerSpec, X, phi0, s, A, B, dY, dX=None, dA=None, dB=None, want_dx=True,
+                   accumulate=False, ws=None, stream=None):
+    """-> (dX or None, dA, dB) with the straight-through estimator; W_hat is recomputed."""
+    T = X.shape[0]
+    m, k, r = spec.out_features, spec.in_features, spec.rank
+    if dX is None and want_dx:
+        dX = torch.empty((T, k), dtype=spec.torch_dtype, device=X.device)
+    if dA is None:
+        dA = torch.empty((m, r), dtype=torch.float32, device=X.device)
+    if dB is None:
+        dB = torch.empty((r, k), dtype=torch.float32, device=X.device)
+    if ws is None:
+        ws = workspace(lrqat_backward_workspace_size(spec, T), X.device)
+    L = spec.c_struct()
+    _check(_lib().lrqat_backward(ctypes.byref(L), T, _ptr(X), _ptr(phi0), _ptr(s), _ptr(A), _ptr(B), _ptr(dY),
+                                 _ptr(dX), _ptr(dA), _ptr(dB), None, int(bool(accumulate)), _ptr(ws), ws.numel(),
+                                 _stream(stream)))
+    return dX, dA, dB
+
+
+def lrqat_merge_to_int4(spec: LayerSpec, phi0, A, B, out=None, stream=None):
+    """W_Z = clip(round(Phi0 + (alpha/r) A B)) double-packed, uint8 [m][k/2]."""
+    if out is None:
+        out = torch.empty((spec.out_features, spec.in_features // 2), dtype=torch.uint8, device=A.device)
+    L = spec.c_struct()
+    _check(_lib().lrqat_merge_to_int4(ctypes.byref(L), _ptr(phi0), _ptr(A), _ptr(B), _ptr(out), _stream(stream)))
+    return out
+
+
+def lrqat_timing_enable(on: bool = True):
+    _lib().lrqat_timing_enable(int(bool(on)))
+
+
+def lrqat_timing_reset():
+    _lib().lrqat_timing_reset()
+
+
+def lrqat_timing_read() -> dict:
+    """{kernel name: (launches, total milliseconds)} since the last reset."""
+    n = 32
+    names = (ctypes.c_char_p * n)()
+    launches = (ctypes.c_int64 * n)()
+    ms = (ctypes.c_double * n)()
+    cnt = _lib().lrqat_timing_read(names, launches, ms, n)
+    if cnt < 0:
+        raise LRQATError(LRQAT_EHIP, "timing read failed")
+    return {names[i].decode(): (int(launches[i]), float(ms[i])) for i in range(cnt)}

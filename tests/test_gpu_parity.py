@@ -1,0 +1,297 @@
+"""GPU parity of the HIP library against the CPU oracle (marked gpu).
+
+Inputs are the seeded synthetic layers of paper_2406_06385_amd.inputs.  Each
+side runs its own setup from W0 (min-max scale, downcast Phi0) and the two
+results are compared bit for bit; the forward/backward outputs are compared
+element by element (small shapes) or on sampled rows/columns (full sizes).
+
+Criteria: integer grid and Phi0/s0/merge bytes bit-exact (a grid element may
+differ only when its pre-round value lies within 1e-5 of a .5 boundary, and
+such elements must stay below a 1e-4 fraction); Y, dX, dA, dB within a
+relative Frobenius error of 1e-4 (float32 activations) or 2e-2 (bfloat16).
+"""
+import sys
+
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+from oracle import lrqat_oracle as O
+from paper_2406_06385_amd import inputs as I
+
+pytestmark = pytest.mark.gpu
+
+TOL = {"fp32": 1e-4, "bf16": 2e-2}
+
+
+def _log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+@pytest.fixture(scope="module")
+def lr():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2406_06385_amd import lrqat
+    lrqat.load_library()
+    return lrqat
+
+
+def rel_fro(dev, ref):
+    dev = np.asarray(dev, np.float64)
+    ref = np.asarray(ref, np.float64)
+    return float(np.linalg.norm(dev - ref) / max(np.linalg.norm(ref), 1e-300))
+
+
+def to_dev_act(a, dtype):
+    if dtype == "bf16":
+        return torch.from_numpy(a.view(np.int16).copy()).view(torch.bfloat16).cuda()
+    return torch.from_numpy(a).cuda()
+
+
+def act_values(a, dtype):
+    """float32 values of an activation array as both sides see them."""
+    return I.bf16_bits_to_fp32(a) if dtype == "bf16" else a
+
+
+def from_dev(t):
+    if t.dtype == torch.bfloat16:
+        return I.bf16_bits_to_fp32(t.view(torch.int16).cpu().numpy().view(np.uint16))
+    return t.cpu().numpy()
+
+
+class Case:
+    """One layer: seeded inputs, both sides' setup, the oracle layer object."""
+
+    def __init__(self, lr, m, k, T, r, alpha, bits, fmt, g=0, act_bits=0, dtype="bf16", seed=7,
+                 b_std=1e-3, outlier_frac=0.0, a_scale=1.0):
+        self.spec = lr.LayerSpec(m, k, r, alpha, bits, fmt, g, act_bits, dtype)
+        self.L = O.Layer(m, k, r, alpha, bits, fmt, g, act_bits)
+        self.dtype = dtype
+        self.T = T
+        self.W0 = I.gen_w0(m, k, seed, seed + 1, 0.02, outlier_frac)
+        self.A = (I.gen_a(m, r, k, seed + 2) * np.float32(a_scale)).astype(np.float32)
+        self.B = I.gen_b(r, k, seed + 3, b_std)
+        self.X = I.gen_act(T, k, seed + 4, 1.0, dtype)
+        self.dY = I.gen_act(T, m, seed + 5, 1e-2, dtype)
+        self.setup(lr)
+
+    @classmethod
+    def from_workload(cls, lr, wl, layer, tokens=None):
+        c = cls.__new__(cls)
+        spec = wl.layers[layer]
+        c.spec = lr.LayerSpec(spec.m, spec.k, wl.rank, wl.alpha, wl.bits, wl.phi_format, wl.group_size,
+                              wl.act_bits, wl.act_dtype)
+        c.L = O.Layer(spec.m, spec.k, wl.rank, wl.alpha, wl.bits, wl.phi_format, wl.group_size, wl.act_bits)
+        c.dtype = wl.act_dtype
+        inp = I.make_layer_inputs(wl, layer, tokens)
+        c.W0, c.A, c.B, c.X, c.dY = inp.W0, inp.A, inp.B, inp.X, inp.dY
+        c.T = c.X.shape[0]
+        c.setup(lr)
+        return c
+
+    def setup(self, lr):
+        L = self.L
+        # oracle side
+        self.s0_ref = O.minmax_scale(self.W0, L.bits, L.group_size)
+        # device side
+        self.d_W0 = torch.from_numpy(self.W0).cuda()
+        self.d_s0, self.d_phi0 = lr.lrqat_init_from_weights(self.spec, self.d_W0)
+        self.phi0_ref = O.encode_phi0(self.W0, self.s0_ref, L.bits, L.fmt, L.group_size)
+        self.d_A = torch.from_numpy(self.A).cuda()
+        self.d_B = torch.from_numpy(self.B).cuda()
+        self.d_X = to_dev_act(self.X, self.dtype)
+        self.d_dY = to_dev_act(self.dY, self.dtype)
+        self.Xv = act_values(self.X, self.dtype)
+        self.dYv = act_values(self.dY, self.dtype).astype(np.float64)
+
+
+def check_setup(c):
+    s0 = c.d_s0.cpu().numpy()
+    phi = c.d_phi0.cpu().numpy()
+    assert np.array_equal(s0.reshape(c.s0_ref.shape), c.s0_ref), "s0 differs from the oracle"
+    assert np.array_equal(phi, c.phi0_ref), f"Phi0 differs in {(phi != c.phi0_ref).sum()} bytes"
+
+
+def check_merge(lr, c, allow_near=False):
+    L = c.L
+    if L.bits > 4:
+        return
+    W = lr.lrqat_merge_to_int4(c.spec, c.d_phi0, c.d_A, c.d_B).cpu().numpy()
+    q_ref, M_ref, near, _ = O.grid_from_inputs(c.phi0_ref, c.A, c.B, L.alpha, L.rank, L.bits, L.fmt)
+    q_dev = O.unpack_int4(W)
+    bad = q_dev != q_ref
+    assert not (bad & ~near).any(), f"{int((bad & ~near).sum())} grid mismatches outside the .5 window"
+    assert bad.sum() < 1e-4 * bad.size
+    if not allow_near:
+        assert np.array_equal(W, O.pack_int4(q_ref)), f"merge bytes differ at {int(bad.sum())} elements"
+    return q_ref, near
+
+
+def run_full(lr, c, accumulate=False):
+    torch.cuda.synchronize()
+    Y = lr.lrqat_forward(c.spec, c.d_X, c.d_phi0, c.d_s0, c.d_A, c.d_B)
+    dA0 = torch.full((c.L.m, c.L.rank), 0.25, device="cuda") if accumulate else None
+    dB0 = torch.full((c.L.rank, c.L.k), -0.5, device="cuda") if accumulate else None
+    dX, dA, dB = lr.lrqat_backward(c.spec, c.d_X, c.d_phi0, c.d_s0, c.d_A, c.d_B, c.d_dY,
+                                   dA=dA0, dB=dB0, accumulate=accumulate)
+    torch.cuda.synchronize()
+    return from_dev(Y), from_dev(dX), dA.cpu().numpy(), dB.cpu().numpy()
+
+
+def check_full(lr, c, accumulate=False):
+    L = c.L
+    Y, dX, dA, dB = run_full(lr, c, accumulate)
+    Yr, _, _, _ = O.forward(L, c.Xv, c.phi0_ref, c.s0_ref, c.A, c.B)
+    gr = O.backward(L, c.Xv, c.phi0_ref, c.s0_ref, c.A, c.B, c.dYv)
+    if accumulate:
+        gr["dA"] = gr["dA"] + 0.25
+        gr["dB"] = gr["dB"] - 0.5
+    tol = TOL[c.dtype]
+    errs = {"Y": rel_fro(Y, Yr), "dX": rel_fro(dX, gr["dX"]), "dA": rel_fro(dA, gr["dA"]), "dB": rel_fro(dB, gr["dB"])}
+    _log(f"  errors {errs}")
+    for k_, e in errs.items():
+        assert e < tol, (k_, e, tol)
+    return errs
+
+
+def check_sampled(lr, c, n_tok=48, n_rows=24, n_cols=24, seed=0):
+    """Full-size run, oracle on sampled token rows (Y, dX), rows of dA, columns of dB."""
+    L = c.L
+    Y, dX, dA, dB = run_full(lr, c)
+    rng = np.random.default_rng(seed)
+    tok = np.unique(np.concatenate([[0, c.T - 1], rng.integers(0, c.T, n_tok)]))
+    rows = np.unique(np.concatenate([[0, L.m - 1], rng.integers(0, L.m, n_rows)]))
+    cols = np.unique(np.concatenate([[0, L.k - 1], rng.integers(0, L.k, n_cols)]))
+    tol = TOL[c.dtype]
+    errs = {
+        "Y": rel_fro(Y[tok], O.forward_rows(L, c.Xv, c.phi0_ref, c.s0_ref, c.A, c.B, tok)),
+        "dX": rel_fro(dX[tok], O.dx_rows(L, c.phi0_ref, c.s0_ref, c.A, c.B, c.dYv, tok)),
+        "dA": rel_fro(dA[rows], O.da_rows(L, c.Xv, c.phi0_ref, c.s0_ref, c.A, c.B, c.dYv, rows)),
+        "dB": rel_fro(dB[:, cols], O.db_cols(L, c.Xv, c.phi0_ref, c.s0_ref, c.A, c.B, c.dYv, cols)),
+    }
+    _log(f"  sampled errors {errs}")
+    for k_, e in errs.items():
+        assert e < tol, (k_, e, tol)
+    assert np.isfinite(Y).all() and np.isfinite(dX).all() and np.isfinite(dA).all() and np.isfinite(dB).all()
+
+
+# ----------------------------------------------------------------------------- the five workloads
+
+@pytest.mark.parametrize("cfg", [1, 2])
+def test_workload_full_or_sampled(lr, cfg):
+    wl = I.WORKLOADS[cfg]
+    _log(f"[workload {cfg}] {wl.name}")
+    c = Case.from_workload(lr, wl, 0)
+    check_setup(c)
+    check_merge(lr, c)
+    if cfg == 1:
+        check_full(lr, c)
+    else:
+        check_sampled(lr, c)
+
+
+@pytest.mark.parametrize("cfg,layer", [(3, 0), (3, 2), (4, 0), (4, 1), (5, 1), (5, 6)])
+def test_workload_sampled_full_size(lr, cfg, layer):
+    wl = I.WORKLOADS[cfg]
+    _log(f"[workload {cfg} layer {wl.layers[layer].name}] m={wl.layers[layer].m} k={wl.layers[layer].k}")
+    c = Case.from_workload(lr, wl, layer)
+    check_setup(c)
+    check_merge(lr, c)
+    check_sampled(lr, c, n_tok=24, n_rows=12, n_cols=12)
+
+
+@pytest.mark.parametrize("cfg", [3, 5])
+def test_workload_merge_all_layers(lr, cfg):
+    wl = I.WORKLOADS[cfg]
+    for layer in range(len(wl.layers)):
+        _log(f"[merge workload {cfg} layer {layer}]")
+        inp = I.make_layer_inputs(wl, layer, with_acts=False)
+        spec = lr.LayerSpec(inp.spec.m, inp.spec.k, wl.rank, wl.alpha, wl.bits, wl.phi_format, wl.group_size,
+                            wl.act_bits, wl.act_dtype)
+        s0, phi0 = lr.lrqat_init_from_weights(spec, torch.from_numpy(inp.W0).cuda())
+        s_ref = O.minmax_scale(inp.W0, wl.bits, wl.group_size)
+        phi_ref = O.encode_phi0(inp.W0, s_ref, wl.bits, wl.phi_format, wl.group_size)
+        assert np.array_equal(phi0.cpu().numpy(), phi_ref)
+        W = lr.lrqat_merge_to_int4(spec, phi0, torch.from_numpy(inp.A).cuda(), torch.from_numpy(inp.B).cuda())
+        L = O.Layer(inp.spec.m, inp.spec.k, wl.rank, wl.alpha, wl.bits, wl.phi_format, wl.group_size, wl.act_bits)
+        assert np.array_equal(W.cpu().numpy(), O.merge_to_int4(L, phi_ref, inp.A, inp.B))
+
+
+# ----------------------------------------------------------------------------- shapes, formats, edge cases
+
+SMALL = [
+    # m, k, T, r, alpha, bits, fmt, g, act, dtype
+    (512, 256, 128, 8, 8.0, 4, "q8", 0, 0, "fp32"),
+    (300, 264, 77, 8, 8.0, 4, "q8", 0, 0, "fp32"),
+    (256, 512, 256, 32, 32.0, 4, "q8", 0, 0, "bf16"),
+    (320, 264, 200, 16, 1.0, 4, "q8", 0, 0, "bf16"),       # ragged m, k, T; alpha = 1
+    (520, 768, 300, 64, 64.0, 3, "q8", 128, 0, "bf16"),    # W3 g128, ragged m and T
+    (384, 640, 96, 32, 32.0, 4, "int_packed2", 0, 0, "bf16"),
+    (384, 640, 333, 32, 32.0, 4, "int_packed2", 0, 8, "bf16"),   # W4A8
+    (200, 96, 64, 1, 1.0, 2, "int_packed2", 0, 0, "bf16"),  # r = 1, INT2
+    (256, 256, 64, 256, 256.0, 4, "q8", 0, 0, "bf16"),      # r = 256
+    (96, 64, 1, 8, 8.0, 2, "q8", 32, 0, "bf16"),            # T = 1, Q2.6, g32
+    (128, 256, 40, 8, 8.0, 3, "q8", 64, 8, "bf16"),
+]
+
+
+@pytest.mark.parametrize("shape", SMALL, ids=[f"m{s[0]}k{s[1]}T{s[2]}r{s[3]}b{s[5]}{s[6]}g{s[7]}a{s[8]}{s[9]}" for s in SMALL])
+def test_small_shapes_full(lr, shape):
+    m, k, T, r, alpha, bits, fmt, g, act, dtype = shape
+    _log(f"[small {shape}]")
+    c = Case(lr, m, k, T, r, alpha, bits, fmt, g, act, dtype, seed=11 + m + k)
+    check_setup(c)
+    check_merge(lr, c)
+    check_full(lr, c)
+
+
+def test_stress_rounding_flips_and_clipping(lr):
+    """B with std 0.3 and a large A flip many roundings and activate the clip."""
+    for fmt, bits in (("q8", 4), ("q8", 3), ("int_packed2", 4)):
+        _log(f"[stress {fmt} b{bits}]")
+        c = Case(lr, 256, 384, 128, 16, 16.0, bits, fmt, 0, 0, "bf16", seed=5, b_std=0.3, a_scale=20.0)
+        check_setup(c)
+        q_ref, near = check_merge(lr, c, allow_near=True)
+        _, M, _, _ = O.grid_from_inputs(c.phi0_ref, c.A, c.B, c.L.alpha, c.L.rank, bits, fmt)
+        assert (~M).sum() > 100, "stress case should clip"
+        check_full(lr, c)
+
+
+def test_accumulate_and_determinism(lr):
+    c = Case(lr, 512, 512, 256, 32, 32.0, 4, "q8", 0, 0, "bf16", seed=3)
+    check_full(lr, c, accumulate=True)
+    a = run_full(lr, c)
+    b = run_full(lr, c)
+    for x, y in zip(a, b):
+        assert np.array_equal(x, y)
+
+
+def test_zero_tokens(lr):
+    spec = lr.LayerSpec(128, 128, 8, 8.0, 4)
+    X = torch.empty((0, 128), dtype=torch.bfloat16, device="cuda")
+    phi = torch.zeros((128, 128), dtype=torch.int8, device="cuda")
+    s = torch.ones(128, device="cuda")
+    A = torch.ones((128, 8), device="cuda")
+    B = torch.ones((8, 128), device="cuda")
+    Y = lr.lrqat_forward(spec, X, phi, s, A, B)
+    assert Y.shape == (0, 128)
+    dA = torch.full((128, 8), 3.0, device="cuda")
+    dB = torch.full((8, 128), 3.0, device="cuda")
+    lr.lrqat_backward(spec, X, phi, s, A, B, torch.empty((0, 128), dtype=torch.bfloat16, device="cuda"),
+                      dA=dA, dB=dB, accumulate=True)
+    torch.cuda.synchronize()
+    assert float(dA.min()) == 3.0 and float(dB.max()) == 3.0
+    lr.lrqat_backward(spec, X, phi, s, A, B, torch.empty((0, 128), dtype=torch.bfloat16, device="cuda"),
+                      dA=dA, dB=dB, accumulate=False)
+    torch.cuda.synchronize()
+    assert float(dA.abs().max()) == 0.0 and float(dB.abs().max()) == 0.0
+
+
+def test_no_dx_requested(lr):
+    c = Case(lr, 256, 256, 64, 8, 8.0, 4, "q8", 0, 0, "bf16", seed=9)
+    _, dA1, dB1 = lr.lrqat_backward(c.spec, c.d_X, c.d_phi0, c.d_s0, c.d_A, c.d_B, c.d_dY, want_dx=False)
+    _, dA2, dB2 = lr.lrqat_backward(c.spec, c.d_X, c.d_phi0, c.d_s0, c.d_A, c.d_B, c.d_dY)
+    torch.cuda.synchronize()
+    assert torch.equal(dA1, dA2) and torch.equal(dB1, dB2)
