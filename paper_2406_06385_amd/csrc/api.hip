@@ -75,6 +75,7 @@ struct Dims {
   int64_t m, k, r, g, ngroups, kpad;
   int bits, packed, act, bf16;
   float c;
+  double c64;
 };
 
 struct Workspace {
@@ -120,6 +121,7 @@ lrqat_status check_layer(const lrqat_layer* L, Dims& d) {
   d.act = L->act_bits == 8;
   d.bf16 = L->act_dtype == LRQAT_BF16;
   d.c = L->alpha / float(L->rank);
+  d.c64 = double(L->alpha) / double(L->rank);
   return LRQAT_OK;
 }
 
@@ -160,6 +162,7 @@ GridArgs grid_args(const Dims& d, const void* phi0, const float* A, const float*
   a.k = d.k;
   a.r = int(d.r);
   a.c = d.c;
+  a.c64 = d.c64;
   a.bits = d.bits;
   a.packed = d.packed;
   a.qout = q;

@@ -78,11 +78,24 @@ __device__ __forceinline__ int tile_off(int r, int c) { return r * 64 + ((c ^ ti
 // resolved to the even one.  float32 keeps the sign of w exact (it is 0 only
 // when the bracket cancels delta exactly), so near the usual decision point
 // w = 0 the only error is that of delta itself.  f = 0 is integer Phi0.
-__host__ __device__ __forceinline__ int grid_round(int code, int f, float delta) {
+__host__ __device__ __forceinline__ int grid_round(int code, int f, float delta, float* margin = nullptr) {
   const int n = code >> f;
   const int cf = code & ((1 << f) - 1);
   const float w = (float(cf) * __builtin_bit_cast(float, uint32_t(127 - f) << 23) - 0.5f) + delta;
   const float cw = __builtin_ceilf(w);
+  int ut = n + int(cw);
+  if (cw == w) ut += ut & 1;
+  if (margin) *margin = __builtin_fabsf(w - __builtin_rintf(w));  // distance to the nearest decision point
+  return ut;
+}
+
+// The same decision with delta in float64, for elements whose float32 margin
+// does not exceed the error bound of the float32 delta.
+__host__ __device__ __forceinline__ int grid_round_f64(int code, int f, double delta) {
+  const int n = code >> f;
+  const int cf = code & ((1 << f) - 1);
+  const double w = (double(cf) * __builtin_bit_cast(double, uint64_t(1023 - f) << 52) - 0.5) + delta;
+  const double cw = __builtin_ceil(w);
   int ut = n + int(cw);
   if (cw == w) ut += ut & 1;
   return ut;

@@ -59,8 +59,12 @@ __global__ __launch_bounds__(256) void k_encode(const float* __restrict__ W0, co
 // ============================================================================ grid
 // Tile 64 rows x 128 columns per block of 4 waves; wave w covers rows
 // 32*(w/2) and columns 64*(w%2) as two 32x32 MFMA blocks.  delta = c A B is
-// an MFMA product of bfloat16 hi/lo splits, A B ~ Ahi Bhi + Ahi Blo + Alo Bhi
-// (relative error ~2^-16 of sum|A||B|), accumulated in float32.
+// an MFMA product of bfloat16 hi/lo splits, A B ~ Ahi Bhi + Ahi Blo + Alo Bhi,
+// accumulated in float32.  Its error is below 3*2^-16 sum_rho |A||B| plus the
+// float32 accumulation, bounded here by 2^-13 |c| max_i ||A_i|| ||B_:j||
+// (Cauchy-Schwarz).  An element whose pre-round value lies within that bound
+// of a rounding decision point is decided again from a float64 delta, so the
+// grid equals the exact one except within float64 rounding of a .5 point.
 constexpr int GR_BM = 64, GR_BN = 128;
 
 // 8 consecutive floats -> bf16 hi part and bf16 lo part (x - hi), packed.
@@ -88,12 +92,14 @@ __global__ __launch_bounds__(256) void k_grid(GridArgs a) {
 
   const int64_t arow = row0 + wr + (lane & 31);
   const int half = lane >> 5;
+  float a2 = 0.f, b2[2] = {0.f, 0.f};  // squared norms: the lane's A row, its B columns
   for (int r0 = 0; r0 < a.r; r0 += 16) {
     // A operand: A[arow][r0 + 8*half + e]
     float x[8];
     for (int e = 0; e < 8; ++e) {
       const int rho = r0 + 8 * half + e;
       x[e] = (arow < a.m && rho < a.r) ? a.A[arow * a.r + rho] : 0.f;
+      a2 += x[e] * x[e];
     }
     u32x4 ahi, alo;
     split8(x, ahi, alo);
@@ -102,6 +108,7 @@ __global__ __launch_bounds__(256) void k_grid(GridArgs a) {
       for (int e = 0; e < 8; ++e) {
         const int rho = r0 + 8 * half + e;
         x[e] = (bcol < a.k && rho < a.r) ? a.B[int64_t(rho) * a.k + bcol] : 0.f;
+        b2[b] += x[e] * x[e];
       }
       u32x4 bhi, blo;
       split8(x, bhi, blo);
@@ -109,6 +116,14 @@ __global__ __launch_bounds__(256) void k_grid(GridArgs a) {
       acc[b] = mfma32(ahi, blo, acc[b]);
       acc[b] = mfma32(alo, bhi, acc[b]);
     }
+  }
+  // the two K-halves of every row / column sit in lanes l and l ^ 32
+  a2 += __shfl_xor(a2, 32);
+  for (int off = 16; off > 0; off >>= 1) a2 = fmaxf(a2, __shfl_xor(a2, off));  // max over the 32 rows
+  float tau[2];
+  for (int b = 0; b < 2; ++b) {
+    b2[b] += __shfl_xor(b2[b], 32);
+    tau[b] = 0x1p-13f * fabsf(a.c) * sqrtf(a2 * b2[b]);
   }
 
   // Rounding decision per element -> LDS as (q & 15) | (in-range ? 0x10 : 0).
@@ -127,7 +142,14 @@ __global__ __launch_bounds__(256) void k_grid(GridArgs a) {
         } else {
           code = int(reinterpret_cast<const int8_t*>(a.phi0)[row * a.ld_phi + col]);
         }
-        const int ut = grid_round(code, f, a.c * acc[b][v]);
+        float margin;
+        int ut = grid_round(code, f, a.c * acc[b][v], &margin);
+        if (margin <= tau[b] + 0x1p-22f) {
+          double d = 0.0;
+          for (int rho = 0; rho < a.r; ++rho)
+            d = __builtin_fma(double(a.A[row * a.r + rho]), double(a.B[int64_t(rho) * a.k + col]), d);
+          ut = grid_round_f64(code, f, a.c64 * d);
+        }
         const int q = min(max(ut, lo), hi);
         cell = uint8_t((q & 15) | (q == ut ? 0x10 : 0));
       }

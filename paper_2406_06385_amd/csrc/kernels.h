@@ -14,6 +14,7 @@ struct GridArgs {
   int64_t m, k;
   int r;
   float c;               // alpha / r
+  double c64;            // alpha / r in float64 (for the exact re-decision)
   int bits;
   int packed;            // 1: Phi0 is double-packed INT-b
   uint8_t* qout;         // packed q [m][ldq]

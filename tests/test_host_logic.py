@@ -64,11 +64,11 @@ def test_grid_round_matches_exact_rne(driver):
     lines = "".join(f"{c} {f} {struct.unpack('<I', struct.pack('<f', float(d)))[0]:x}\n" for c, f, d in cases)
     r = subprocess.run([driver], input=lines, capture_output=True, text=True)
     assert r.returncode == 0
-    got = [int(t) for t in r.stdout.split()]
+    got = [tuple(int(t) for t in line.split()) for line in r.stdout.splitlines()]
     assert len(got) == len(cases)
     bad = []
-    for (c, f, d), g in zip(cases, got):
+    for (c, f, d), (g32, g64) in zip(cases, got):
         want = _rne(Fraction(c, 2 ** f) + Fraction(float(d)))
-        if g != want:
-            bad.append((c, f, float(d), g, want))
+        if g32 != want or g64 != want:
+            bad.append((c, f, float(d), g32, g64, want))
     assert not bad, bad[:10]
