@@ -66,7 +66,7 @@ hipError_t timed(const char* name, hipStream_t st, F&& launch) {
 }
 
 // ------------------------------------------------------------------ layout
-constexpr int64_t kMaxDim = int64_t(1) << 30;
+constexpr int64_t kMaxDim = int64_t(1) << 22;  // keeps 32-bit buffer offsets within a 256-row tile
 
 inline int64_t round_up(int64_t x, int64_t a) { return (x + a - 1) / a * a; }
 inline bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }

@@ -47,6 +47,7 @@ __global__ __launch_bounds__(256) void k_encode(const float* __restrict__ W0, co
     static_cast<int8_t*>(phi0)[row * k + col] = int8_t(int(__builtin_rintf(xc * float(1 << f))));
   } else {
     int v[2];
+    #pragma unroll
     for (int e = 0; e < 2; ++e) {
       const int64_t j = 2 * col + e;
       const float x = W0[row * k + j] / s0[row * ngroups + j / gsize];
@@ -69,6 +70,7 @@ constexpr int GR_BM = 64, GR_BN = 128;
 
 // 8 consecutive floats -> bf16 hi part and bf16 lo part (x - hi), packed.
 __device__ __forceinline__ void split8(const float (&x)[8], u32x4& hi, u32x4& lo) {
+  #pragma unroll
   for (int p = 0; p < 4; ++p) {
     const uint32_t h = pack_bf16x2(x[2 * p], x[2 * p + 1]);
     hi[p] = h;
@@ -87,7 +89,9 @@ __global__ __launch_bounds__(256) void k_grid(GridArgs a) {
   const int f = a.packed ? 0 : 8 - a.bits;
 
   f32x16 acc[2];
+  #pragma unroll
   for (int b = 0; b < 2; ++b)
+    #pragma unroll
     for (int v = 0; v < 16; ++v) acc[b][v] = 0.f;
 
   const int64_t arow = row0 + wr + (lane & 31);
@@ -96,6 +100,7 @@ __global__ __launch_bounds__(256) void k_grid(GridArgs a) {
   for (int r0 = 0; r0 < a.r; r0 += 16) {
     // A operand: A[arow][r0 + 8*half + e]
     float x[8];
+    #pragma unroll
     for (int e = 0; e < 8; ++e) {
       const int rho = r0 + 8 * half + e;
       x[e] = (arow < a.m && rho < a.r) ? a.A[arow * a.r + rho] : 0.f;
@@ -103,8 +108,10 @@ __global__ __launch_bounds__(256) void k_grid(GridArgs a) {
     }
     u32x4 ahi, alo;
     split8(x, ahi, alo);
+    #pragma unroll
     for (int b = 0; b < 2; ++b) {
       const int64_t bcol = col0 + wc + 32 * b + (lane & 31);
+      #pragma unroll
       for (int e = 0; e < 8; ++e) {
         const int rho = r0 + 8 * half + e;
         x[e] = (bcol < a.k && rho < a.r) ? a.B[int64_t(rho) * a.k + bcol] : 0.f;
@@ -121,15 +128,18 @@ __global__ __launch_bounds__(256) void k_grid(GridArgs a) {
   a2 += __shfl_xor(a2, 32);
   for (int off = 16; off > 0; off >>= 1) a2 = fmaxf(a2, __shfl_xor(a2, off));  // max over the 32 rows
   float tau[2];
+  #pragma unroll
   for (int b = 0; b < 2; ++b) {
     b2[b] += __shfl_xor(b2[b], 32);
     tau[b] = 0x1p-13f * fabsf(a.c) * sqrtf(a2 * b2[b]);
   }
 
   // Rounding decision per element -> LDS as (q & 15) | (in-range ? 0x10 : 0).
+  #pragma unroll
   for (int b = 0; b < 2; ++b) {
     const int lc = wc + 32 * b + (lane & 31);
     const int64_t col = col0 + lc;
+    #pragma unroll
     for (int v = 0; v < 16; ++v) {
       const int lr = wr + acc_row(v, lane);
       const int64_t row = row0 + lr;
@@ -165,8 +175,10 @@ __global__ __launch_bounds__(256) void k_grid(GridArgs a) {
     const int64_t cbase = col0 + 32 * seg;          // first column of this segment
     if (row < a.m && cbase < a.kq) {
       uint32_t w[4];
+      #pragma unroll
       for (int p = 0; p < 4; ++p) {
         uint32_t acc_w = 0;
+        #pragma unroll
         for (int e = 0; e < 8; ++e) acc_w |= uint32_t(qs[lr][32 * seg + 8 * p + e] & 15) << (4 * e);
         w[p] = acc_w;
       }
@@ -186,6 +198,7 @@ __global__ __launch_bounds__(256) void k_grid(GridArgs a) {
     const int64_t cbase = col0 + 32 * seg;
     if (row < a.m && cbase < a.kq) {
       uint32_t bitsw = 0;
+      #pragma unroll
       for (int e = 0; e < 32; ++e) bitsw |= uint32_t((qs[lr][32 * seg + e] >> 4) & 1) << e;
       *reinterpret_cast<uint32_t*>(a.mout + row * a.ldm + (cbase >> 3)) = bitsw;
     }
