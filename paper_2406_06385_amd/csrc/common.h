@@ -59,15 +59,6 @@ __device__ __forceinline__ f32x16 mfma32(const u32x4& a, const u32x4& b, const f
 }
 __device__ __forceinline__ int acc_row(int v, int lane) { return 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3); }
 
-// ---------------------------------------------------------------- LDS tiles
-// Operand tiles are [rows][64] bfloat16 (128-byte rows of eight 16-byte
-// chunks).  Chunk c of row r lives at chunk position c ^ swz(r): eight
-// consecutive rows read at one chunk position hit eight different bank
-// groups, and so do sixteen consecutive rows for 256-byte bank windows.
-__device__ __forceinline__ int tile_swz(int r) { return (r & 7) ^ ((r >> 3) & 7); }
-// Element offset of chunk c (0..7) of row r.
-__device__ __forceinline__ int tile_off(int r, int c) { return r * 64 + ((c ^ tile_swz(r)) << 3); }
-
 // ---------------------------------------------------------------- the grid decision
 // round-half-even(u) for u = code * 2^-f + delta, taken without absorbing a
 // small delta into the stored value.  With n = floor(code / 2^f) and the

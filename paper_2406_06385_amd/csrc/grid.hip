@@ -78,8 +78,14 @@ __device__ __forceinline__ void split8(const float (&x)[8], u32x4& hi, u32x4& lo
   }
 }
 
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t grid_rsrc(const void* base, int64_t bytes) {
+  const int64_t n = bytes < 0 ? 0 : (bytes > int64_t(0xFFFFFFFF) ? int64_t(0xFFFFFFFF) : bytes);
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), short(0), int(uint32_t(n)), 0x00020000);
+}
+
 __global__ __launch_bounds__(256) void k_grid(GridArgs a) {
-  __shared__ uint8_t qs[GR_BM][GR_BN];  // (q & 15) | 0x10 when the element is inside the grid
+  __shared__ uint8_t qs[GR_BM][GR_BN];     // (q & 15) | 0x10 when the element is inside the grid
+  __shared__ uint8_t ph[GR_BM][GR_BN];     // the block's Phi0 bytes (GR_BN/2 per row when packed)
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int64_t ncb = (a.kq + GR_BN - 1) / GR_BN;
   const int64_t row0 = int64_t(blockIdx.x / ncb) * GR_BM;
@@ -88,33 +94,62 @@ __global__ __launch_bounds__(256) void k_grid(GridArgs a) {
   const int lo = -(1 << (a.bits - 1)), hi = (1 << (a.bits - 1)) - 1;
   const int f = a.packed ? 0 : 8 - a.bits;
 
+  // Stage the Phi0 tile in LDS first so its loads overlap the rank-r product.
+  // Rows past m read as zeros (buffer range); columns past k are never used.
+  {
+    const int64_t bpr = a.packed ? GR_BN / 2 : GR_BN;          // bytes per tile row
+    const int64_t cb0 = a.packed ? col0 / 2 : col0;
+    const auto r = grid_rsrc(a.phi0 + row0 * a.ld_phi + cb0, (a.m - row0) * a.ld_phi - cb0);
+    const int tr = threadIdx.x >> 2, seg = threadIdx.x & 3;   // 4 threads per row
+    const int64_t nbytes = bpr / 4;                            // 32 (fixed point) or 16 (packed)
+    if ((a.ld_phi & 15) == 0) {
+      for (int64_t o = 0; o < nbytes; o += 16) {
+        const u32x4 v = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
+            r, int(tr * a.ld_phi + seg * nbytes + o), 0, 0));
+        *reinterpret_cast<u32x4*>(&ph[tr][seg * nbytes + o]) = v;
+      }
+    } else {
+      for (int64_t o = 0; o < nbytes; ++o)
+        ph[tr][seg * nbytes + o] = uint8_t(__builtin_amdgcn_raw_buffer_load_b8(r, int(tr * a.ld_phi + seg * nbytes + o), 0, 0));
+    }
+  }
+
   f32x16 acc[2];
-  #pragma unroll
+#pragma unroll
   for (int b = 0; b < 2; ++b)
-    #pragma unroll
+#pragma unroll
     for (int v = 0; v < 16; ++v) acc[b][v] = 0.f;
 
   const int64_t arow = row0 + wr + (lane & 31);
   const int half = lane >> 5;
+  const bool avec = (a.r & 3) == 0 && (reinterpret_cast<uintptr_t>(a.A) & 15) == 0;
   float a2 = 0.f, b2[2] = {0.f, 0.f};  // squared norms: the lane's A row, its B columns
   for (int r0 = 0; r0 < a.r; r0 += 16) {
     // A operand: A[arow][r0 + 8*half + e]
     float x[8];
-    #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const int rho = r0 + 8 * half + e;
-      x[e] = (arow < a.m && rho < a.r) ? a.A[arow * a.r + rho] : 0.f;
-      a2 += x[e] * x[e];
+    const int rb = r0 + 8 * half;
+    if (avec && arow < a.m && rb + 8 <= a.r) {
+      const f32x4 u = *reinterpret_cast<const f32x4*>(a.A + arow * a.r + rb);
+      const f32x4 w = *reinterpret_cast<const f32x4*>(a.A + arow * a.r + rb + 4);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        x[e] = u[e];
+        x[4 + e] = w[e];
+      }
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) x[e] = (arow < a.m && rb + e < a.r) ? a.A[arow * a.r + rb + e] : 0.f;
     }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) a2 += x[e] * x[e];
     u32x4 ahi, alo;
     split8(x, ahi, alo);
-    #pragma unroll
+#pragma unroll
     for (int b = 0; b < 2; ++b) {
       const int64_t bcol = col0 + wc + 32 * b + (lane & 31);
-      #pragma unroll
+#pragma unroll
       for (int e = 0; e < 8; ++e) {
-        const int rho = r0 + 8 * half + e;
-        x[e] = (bcol < a.k && rho < a.r) ? a.B[int64_t(rho) * a.k + bcol] : 0.f;
+        x[e] = (bcol < a.k && rb + e < a.r) ? a.B[int64_t(rb + e) * a.k + bcol] : 0.f;
         b2[b] += x[e] * x[e];
       }
       u32x4 bhi, blo;
@@ -128,42 +163,42 @@ __global__ __launch_bounds__(256) void k_grid(GridArgs a) {
   a2 += __shfl_xor(a2, 32);
   for (int off = 16; off > 0; off >>= 1) a2 = fmaxf(a2, __shfl_xor(a2, off));  // max over the 32 rows
   float tau[2];
-  #pragma unroll
+#pragma unroll
   for (int b = 0; b < 2; ++b) {
     b2[b] += __shfl_xor(b2[b], 32);
     tau[b] = 0x1p-13f * fabsf(a.c) * sqrtf(a2 * b2[b]);
   }
+  __syncthreads();  // Phi0 tile staged
 
   // Rounding decision per element -> LDS as (q & 15) | (in-range ? 0x10 : 0).
-  #pragma unroll
+#pragma unroll
   for (int b = 0; b < 2; ++b) {
     const int lc = wc + 32 * b + (lane & 31);
     const int64_t col = col0 + lc;
-    #pragma unroll
+#pragma unroll
     for (int v = 0; v < 16; ++v) {
       const int lr = wr + acc_row(v, lane);
       const int64_t row = row0 + lr;
-      uint8_t cell = 0;
-      if (row < a.m && col < a.k) {
-        int code;
-        if (a.packed) {
-          const uint8_t byte = a.phi0[row * a.ld_phi + (col >> 1)];
-          code = int(uint32_t(byte) << (28 - 4 * int(col & 1))) >> 28;
-        } else {
-          code = int(reinterpret_cast<const int8_t*>(a.phi0)[row * a.ld_phi + col]);
+      int code;
+      if (a.packed) code = int(uint32_t(ph[lr][lc >> 1]) << (28 - 4 * (lc & 1))) >> 28;
+      else code = int(int8_t(ph[lr][lc]));
+      float margin;
+      int ut = grid_round(code, f, a.c * acc[b][v], &margin);
+      if (margin <= tau[b] && row < a.m && col < a.k) {
+        // float64 re-decision; independent partial sums keep the loads in flight
+        double d0 = 0.0, d1 = 0.0, d2 = 0.0, d3 = 0.0;
+        int rho = 0;
+        for (; rho + 4 <= a.r; rho += 4) {
+          d0 = __builtin_fma(double(a.A[row * a.r + rho]), double(a.B[int64_t(rho) * a.k + col]), d0);
+          d1 = __builtin_fma(double(a.A[row * a.r + rho + 1]), double(a.B[int64_t(rho + 1) * a.k + col]), d1);
+          d2 = __builtin_fma(double(a.A[row * a.r + rho + 2]), double(a.B[int64_t(rho + 2) * a.k + col]), d2);
+          d3 = __builtin_fma(double(a.A[row * a.r + rho + 3]), double(a.B[int64_t(rho + 3) * a.k + col]), d3);
         }
-        float margin;
-        int ut = grid_round(code, f, a.c * acc[b][v], &margin);
-        if (margin <= tau[b] + 0x1p-22f) {
-          double d = 0.0;
-          for (int rho = 0; rho < a.r; ++rho)
-            d = __builtin_fma(double(a.A[row * a.r + rho]), double(a.B[int64_t(rho) * a.k + col]), d);
-          ut = grid_round_f64(code, f, a.c64 * d);
-        }
-        const int q = min(max(ut, lo), hi);
-        cell = uint8_t((q & 15) | (q == ut ? 0x10 : 0));
+        for (; rho < a.r; ++rho) d0 = __builtin_fma(double(a.A[row * a.r + rho]), double(a.B[int64_t(rho) * a.k + col]), d0);
+        ut = grid_round_f64(code, f, a.c64 * ((d0 + d1) + (d2 + d3)));
       }
-      qs[lr][lc] = cell;
+      const int q = min(max(ut, lo), hi);
+      qs[lr][lc] = (row < a.m && col < a.k) ? uint8_t((q & 15) | (q == ut ? 0x10 : 0)) : uint8_t(0);
     }
   }
   __syncthreads();
