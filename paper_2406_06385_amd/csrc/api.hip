@@ -72,7 +72,7 @@ inline int64_t round_up(int64_t x, int64_t a) { return (x + a - 1) / a * a; }
 inline bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
 
 struct Dims {
-  int64_t m, k, r, g, ngroups, kpad;
+  int64_t m, k, r, g, ngroups, kpad, mpad;
   int bits, packed, act, bf16;
   float c;
   double c64;
@@ -116,6 +116,7 @@ lrqat_status check_layer(const lrqat_layer* L, Dims& d) {
   d.g = L->group_size;
   d.ngroups = d.g ? d.k / d.g : 1;
   d.kpad = round_up(d.k, GEMM_BN);
+  d.mpad = round_up(d.m, GEMM_BM);
   d.bits = L->bits;
   d.packed = L->phi_format == LRQAT_PHI_INT_PACKED2;
   d.act = L->act_bits == 8;
@@ -134,7 +135,7 @@ Workspace layout(const Dims& d, int64_t T, bool backward) {
     return at;
   };
   w.q = take(size_t(d.m * d.kpad / 2));
-  if (backward) w.mask = take(size_t(d.m * d.kpad / 8));
+  if (backward) w.mask = take(size_t(d.kpad * d.mpad / 8));
   if (d.act) {
     w.n = take(size_t(T * d.kpad));
     w.sx = take(size_t(T * 4));
@@ -169,7 +170,7 @@ GridArgs grid_args(const Dims& d, const void* phi0, const float* A, const float*
   a.ldq = d.kpad / 2;
   a.kq = d.kpad;
   a.mout = mask;
-  a.ldm = d.kpad / 8;
+  a.ldm = d.mpad / 8;
   return a;
 }
 
@@ -321,7 +322,7 @@ lrqat_status lrqat_backward(const lrqat_layer* layer, int64_t tokens, const void
     fa.X = static_cast<const float*>(X);
     fa.dY = static_cast<const float*>(dY);
     fa.q = q; fa.ldq = d.kpad / 2;
-    fa.mask = mask; fa.ldm = d.kpad / 8;
+    fa.mask = mask; fa.ldm = d.mpad / 8;
     fa.s = s; fa.gsize = d.g; fa.ngroups = d.ngroups;
     fa.A = A; fa.B = B;
     fa.G = reinterpret_cast<float*>(base + w.G);
@@ -355,7 +356,7 @@ lrqat_status lrqat_backward(const lrqat_layer* layer, int64_t tokens, const void
   p.ldb = d.act ? d.kpad : d.k;
   p.s = s; p.gsize = d.g; p.ngroups = d.ngroups;
   p.sx = d.act ? sx : nullptr;
-  p.mask = mask; p.ldm = d.kpad / 8;
+  p.mask = mask; p.ldm = d.mpad / 8;
   p.Am = A; p.Bm = B; p.r = int(d.r);
   p.dA_part = dA_part; p.dB_part = dB_part;
   LRQAT_TRY(hip_status(timed("gemm_dw", st, [&] { return launch_gemm(kDw, d.act, d.g != 0, p, st); }), "gemm_dw"));

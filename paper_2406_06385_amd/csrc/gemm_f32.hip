@@ -83,7 +83,7 @@ struct StoreG {  // G = s * M * dW
   const float* s;
   int64_t gsize, ngroups;
   __device__ void operator()(int64_t i, int64_t j, float v) const {
-    const int bit = (mask[i * ldm + (j >> 3)] >> (j & 7)) & 1;
+    const int bit = (mask[j * ldm + (i >> 3)] >> (i & 7)) & 1;
     const float sc = gsize ? s[i * ngroups + j / gsize] : s[i];
     g[i * k + j] = bit ? v * sc : 0.f;
   }

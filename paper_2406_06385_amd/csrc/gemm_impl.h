@@ -1,0 +1,656 @@
+// bf16 MFMA GEMMs of the LR-QAT layer on gfx950.
+//
+//   kFwd  Y  = X_hat W_hat^T      M = T, N = m, K = k   (Section 3, Eq. lr_qat)
+//   kDx   dX = dY W_hat           M = T, N = k, K = m
+//   kDw   dW = dY^T X_hat         M = m, N = k, K = T, never stored: the
+//         epilogue forms G = s * M * dW and the rank-r partial products
+//         G B^T and A^T G (Section 3, STE gradients w.r.t. A and B).
+//
+// W_hat enters as the packed integer grid q written by the grid pass; the
+// operand loaders unpack it into bfloat16 tiles in LDS (exact for |q| <= 8),
+// with the scale s applied in the epilogue (forward, per channel) or folded
+// into the tile (dX, and the forward with group-wise scales).
+//
+// Block tile 256 x 256 x 64, four waves in a 2 x 2 arrangement, each wave a
+// 128 x 128 sub-tile of 4 x 4 MFMA 32x32x16 blocks.  Two LDS stages of
+// (256 + 256) x 64 bfloat16 (128 KiB); the next K-tile is fetched into
+// registers while the current one feeds the MFMAs.
+#pragma once
+
+#include "kernels.h"
+
+namespace lrqat {
+
+constexpr int BM = GEMM_BM, BN = GEMM_BN, BK = GEMM_BK;
+// Operand tiles in LDS are [256 rows][64] bfloat16 (128-byte rows of eight
+// 16-byte chunks).  Chunk c of row r sits at chunk slot c ^ g(r) with
+// g(r) = (r & 7) ^ ((r >> 3) & 1): any 8 consecutive rows read at one chunk
+// hit 8 different slots (32 banks), any 16 consecutive rows hit 16 different
+// (row parity, slot) pairs (64 banks).  g depends on r mod 16 only, so the
+// fragments of row blocks 32 apart are constant offsets of one address.
+constexpr int TILE = 256 * 64;  // elements of one operand tile
+__device__ __forceinline__ int tile_g(int row) { return (row & 7) ^ ((row >> 3) & 1); }
+__device__ __forceinline__ int tile_off(int row, int chunk) { return row * 64 + ((chunk ^ tile_g(row)) << 3); }
+
+// ------------------------------------------------------------------ buffer resources
+// Operands are read with raw buffer loads.  A load whose per-lane offset is
+// at or past the resource's num_records returns zeros, so a tile that
+// overhangs the end of a tensor needs no per-lane branch: each resource
+// starts at the tile's origin and all strides stay in the per-lane offset.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void* base, int64_t bytes) {
+  const int64_t n = bytes < 0 ? 0 : (bytes > int64_t(0xFFFFFFFF) ? int64_t(0xFFFFFFFF) : bytes);
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), short(0), int(uint32_t(n)), 0x00020000);
+}
+__device__ __forceinline__ u32x4 ld128(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, int(off), 0, 0));
+}
+__device__ __forceinline__ u32x2 ld64(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(r, int(off), 0, 0));
+}
+__device__ __forceinline__ uint32_t ld32(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __builtin_amdgcn_raw_buffer_load_b32(r, int(off), 0, 0);
+}
+__device__ __forceinline__ uint32_t ld16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __builtin_amdgcn_raw_buffer_load_b16(r, int(off), 0, 0);
+}
+__device__ __forceinline__ float ldf(__amdgpu_buffer_rsrc_t r, uint32_t off) { return __uint_as_float(ld32(r, off)); }
+
+// 8 bfloat16 starting at byte offset `off` with 16-bit loads (rows not 16-byte aligned).
+__device__ __forceinline__ u32x4 ld8_bf16_scalar(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  u32x4 v;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) v[q] = ld16(r, off + 4 * q) | (ld16(r, off + 4 * q + 2) << 16);
+  return v;
+}
+
+// Zero the elements of an 8-wide bfloat16 chunk at column kk that lie at or past K.
+__device__ __forceinline__ u32x4 mask_tail(u32x4 v, int kk, int K) {
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const uint32_t lo = (kk + 2 * q < K) ? 0x0000FFFFu : 0u, hi = (kk + 2 * q + 1 < K) ? 0xFFFF0000u : 0u;
+    v[q] &= lo | hi;
+  }
+  return v;
+}
+
+// ------------------------------------------------------------------ K-contiguous bf16 source
+// 256 x 64 tile of a row-major [rows][K] bfloat16 matrix (forward X, dX's dY);
+// thread t loads chunk t%8 of rows t/8 + 32 i.
+struct RegsKc {
+  u32x4 v[8];
+  int kk;      // first column of the thread's chunk (columns >= K are masked on the generic path)
+};
+
+template <bool VEC>
+__device__ __forceinline__ void load_kc_bf16(RegsKc& R, const uint16_t* __restrict__ src, int64_t ld,
+                                             int64_t row0, int64_t nrows, int64_t k0, int64_t K) {
+  const int t = threadIdx.x;
+  const auto r = rsrc(src + row0 * ld, (nrows - row0) * ld * 2);
+  R.kk = int(k0) + 8 * (t & 7);
+  const uint32_t base = uint32_t(((t >> 3) * ld + R.kk) * 2), step = uint32_t(32 * ld * 2);
+#pragma unroll
+  for (int i = 0; i < 8; ++i) R.v[i] = VEC ? ld128(r, base + i * step) : ld8_bf16_scalar(r, base + i * step);
+}
+
+template <bool VEC>
+__device__ __forceinline__ void store_kc(uint16_t* tile, const RegsKc& R, int64_t K) {
+  const int t = threadIdx.x;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    u32x4 v = R.v[i];
+    if (!VEC) v = mask_tail(v, R.kk, int(K));
+    *reinterpret_cast<u32x4*>(tile + tile_off((t >> 3) + 32 * i, t & 7)) = v;
+  }
+}
+
+// ------------------------------------------------------------------ K-contiguous int8 source (W4A8 codes)
+// n [T][ld] is zero beyond column k, so no K mask is needed.
+struct RegsKc8 {
+  u32x2 v[8];
+};
+
+__device__ __forceinline__ void load_kc_i8(RegsKc8& R, const int8_t* __restrict__ src, int64_t ld,
+                                           int64_t row0, int64_t nrows, int64_t k0) {
+  const int t = threadIdx.x;
+  const auto r = rsrc(src + row0 * ld, (nrows - row0) * ld);
+  const uint32_t base = uint32_t((t >> 3) * ld + k0 + 8 * (t & 7)), step = uint32_t(32 * ld);
+#pragma unroll
+  for (int i = 0; i < 8; ++i) R.v[i] = ld64(r, base + i * step);
+}
+
+__device__ __forceinline__ void store_kc_i8(uint16_t* tile, const RegsKc8& R) {
+  const int t = threadIdx.x;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    u32x4 o;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const uint32_t w = R.v[i][q >> 1];
+      o[q] = pack_bf16x2(float(sbyte(w, 2 * (q & 1))), float(sbyte(w, 2 * (q & 1) + 1)));
+    }
+    *reinterpret_cast<u32x4*>(tile + tile_off((t >> 3) + 32 * i, t & 7)) = o;
+  }
+}
+
+// ------------------------------------------------------------------ packed q, K-contiguous (forward B)
+// 256 weight rows x 64 K-values = 256 x 32 bytes; thread t takes 16 bytes
+// (32 values) of rows t/2 and t/2 + 128.  q is zero past column k.
+struct RegsQKc {
+  u32x4 v[2];
+  float sc[2];
+};
+
+template <bool GRP>
+__device__ __forceinline__ void load_q_kc(RegsQKc& R, const GemmArgs& p, int64_t row0, int64_t k0) {
+  const int t = threadIdx.x;
+  const int64_t kk = k0 + 32 * (t & 1);
+  const auto rq = rsrc(static_cast<const uint8_t*>(p.b) + row0 * p.ldb, (p.N - row0) * p.ldb);
+  const uint32_t base = uint32_t((t >> 1) * p.ldb + (kk >> 1)), step = uint32_t(128 * p.ldb);
+#pragma unroll
+  for (int i = 0; i < 2; ++i) R.v[i] = ld128(rq, base + i * step);
+  if (GRP) {
+    const auto rs = rsrc(p.s + row0 * p.ngroups, (p.N - row0) * p.ngroups * 4);
+    const uint32_t sb = uint32_t(((t >> 1) * p.ngroups + kk / p.gsize) * 4), sstep = uint32_t(128 * p.ngroups * 4);
+#pragma unroll
+    for (int i = 0; i < 2; ++i) R.sc[i] = ldf(rs, sb + i * sstep);
+  }
+}
+
+template <bool GRP>
+__device__ __forceinline__ void store_q_kc(uint16_t* tile, const RegsQKc& R) {
+  const int t = threadIdx.x;
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int row = (t >> 1) + 128 * i;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const uint32_t w = R.v[i][c];
+      u32x4 o;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        float a = float(nibble(w, 2 * q)), b = float(nibble(w, 2 * q + 1));
+        if (GRP) {
+          a *= R.sc[i];
+          b *= R.sc[i];
+        }
+        o[q] = pack_bf16x2(a, b);
+      }
+      *reinterpret_cast<u32x4*>(tile + tile_off(row, 4 * (t & 1) + c)) = o;
+    }
+  }
+}
+
+// ------------------------------------------------------------------ K-strided sources
+// Tile rows are the index contiguous in memory, K the strided one.  Thread t
+// covers 8 consecutive tile rows 8 (t/8) .. +7 (one vector per K-line) of
+// the 8 K-lines 8 (t%8) .. +7 and transposes them in registers into 8
+// chunks; the 8 lanes of a K-group fill one 128-byte row segment of LDS.
+// Columns past a tensor's width only feed output rows/columns that the
+// epilogue discards; K-lines past the end read as zeros.
+
+// packed q (dX B): K = weight rows (m), tile rows = weight columns (k).
+// Values are scaled by their row's (or row-group's) s before rounding to bf16.
+struct RegsQKs {
+  uint32_t w[8];
+  float sc[8];
+};
+
+template <bool GRP>
+__device__ __forceinline__ void load_q_ks(RegsQKs& R, const GemmArgs& p, int64_t n0, int64_t k0) {
+  const int t = threadIdx.x;
+  const int kg = t & 7, a = t >> 3;
+  const int64_t col = n0 + 8 * a;
+  const auto rq = rsrc(static_cast<const uint8_t*>(p.b) + k0 * p.ldb, (p.K - k0) * p.ldb);
+  const uint32_t base = uint32_t(8 * kg * p.ldb + (col >> 1)), step = uint32_t(p.ldb);
+#pragma unroll
+  for (int e = 0; e < 8; ++e) R.w[e] = ld32(rq, base + e * step);
+  if (GRP) {
+    const auto rs = rsrc(p.s + k0 * p.ngroups, (p.K - k0) * p.ngroups * 4);
+    const uint32_t sb = uint32_t((8 * kg * p.ngroups + col / p.gsize) * 4), sstep = uint32_t(p.ngroups * 4);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) R.sc[e] = ldf(rs, sb + e * sstep);
+  } else {
+    const auto rs = rsrc(p.s + k0, (p.K - k0) * 4);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) R.sc[e] = ldf(rs, uint32_t((8 * kg + e) * 4));
+  }
+}
+
+__device__ __forceinline__ void store_q_ks(uint16_t* tile, const RegsQKs& R) {
+  const int t = threadIdx.x;
+  const int kg = t & 7, a = t >> 3;
+#pragma unroll
+  for (int c = 0; c < 8; ++c) {
+    u32x4 o;
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      o[q] = pack_bf16x2(float(nibble(R.w[2 * q], c)) * R.sc[2 * q],
+                         float(nibble(R.w[2 * q + 1], c)) * R.sc[2 * q + 1]);
+    *reinterpret_cast<u32x4*>(tile + tile_off(8 * a + c, kg)) = o;
+  }
+}
+
+// bfloat16 (dW A = dY, dW B = X): 16-byte vector per K-line.
+struct RegsKs {
+  u32x4 v[8];
+};
+
+template <bool VEC>
+__device__ __forceinline__ void load_ks_bf16(RegsKs& R, const uint16_t* __restrict__ src, int64_t ld,
+                                             int64_t c0, int64_t k0, int64_t K) {
+  const int t = threadIdx.x;
+  const int kg = t & 7, a = t >> 3;
+  const auto r = rsrc(src + k0 * ld + c0, (K - k0) * ld * 2 - c0 * 2);
+  const uint32_t base = uint32_t((8 * kg * ld + 8 * a) * 2), step = uint32_t(ld * 2);
+#pragma unroll
+  for (int e = 0; e < 8; ++e) R.v[e] = VEC ? ld128(r, base + e * step) : ld8_bf16_scalar(r, base + e * step);
+}
+
+__device__ __forceinline__ void store_ks_bf16(uint16_t* tile, const RegsKs& R) {
+  const int t = threadIdx.x;
+  const int kg = t & 7, a = t >> 3;
+#pragma unroll
+  for (int c = 0; c < 8; ++c) {
+    u32x4 o;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const uint32_t x = R.v[2 * q][c >> 1], y = R.v[2 * q + 1][c >> 1];
+      o[q] = (c & 1) ? perm_hi16(x, y) : perm_lo16(x, y);
+    }
+    *reinterpret_cast<u32x4*>(tile + tile_off(8 * a + c, kg)) = o;
+  }
+}
+
+// int8 codes n [T][ld] times s_x[t] (dW B under W4A8).
+struct RegsKs8 {
+  u32x2 v[8];
+  float sx[8];
+};
+
+__device__ __forceinline__ void load_ks_i8(RegsKs8& R, const int8_t* __restrict__ src, int64_t ld,
+                                           const float* __restrict__ sx, int64_t c0, int64_t k0, int64_t K) {
+  const int t = threadIdx.x;
+  const int kg = t & 7, a = t >> 3;
+  const auto r = rsrc(src + k0 * ld + c0, (K - k0) * ld - c0);
+  const auto rs = rsrc(sx + k0, (K - k0) * 4);
+  const uint32_t base = uint32_t(8 * kg * ld + 8 * a), step = uint32_t(ld);
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    R.v[e] = ld64(r, base + e * step);
+    R.sx[e] = ldf(rs, uint32_t((8 * kg + e) * 4));
+  }
+}
+
+__device__ __forceinline__ void store_ks_i8(uint16_t* tile, const RegsKs8& R) {
+  const int t = threadIdx.x;
+  const int kg = t & 7, a = t >> 3;
+#pragma unroll
+  for (int c = 0; c < 8; ++c) {
+    u32x4 o;
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      o[q] = pack_bf16x2(float(sbyte(R.v[2 * q][c >> 2], c & 3)) * R.sx[2 * q],
+                         float(sbyte(R.v[2 * q + 1][c >> 2], c & 3)) * R.sx[2 * q + 1]);
+    *reinterpret_cast<u32x4*>(tile + tile_off(8 * a + c, kg)) = o;
+  }
+}
+
+// ------------------------------------------------------------------ the kernel
+
+template <int V, bool ACT, bool GRP, bool VEC>
+struct Loader;
+
+template <bool ACT, bool GRP, bool VEC>
+struct Loader<kFwd, ACT, GRP, VEC> {
+  typename std::conditional<ACT, RegsKc8, RegsKc>::type ra;
+  RegsQKc rb;
+  __device__ __forceinline__ void load(const GemmArgs& p, int64_t m0, int64_t n0, int64_t k0) {
+    if constexpr (ACT) load_kc_i8(ra, static_cast<const int8_t*>(p.a), p.lda, m0, p.M, k0);
+    else load_kc_bf16<VEC>(ra, static_cast<const uint16_t*>(p.a), p.lda, m0, p.M, k0, p.K);
+    load_q_kc<GRP>(rb, p, n0, k0);
+  }
+  __device__ __forceinline__ void store(const GemmArgs& p, uint16_t* As, uint16_t* Bs) {
+    if constexpr (ACT) store_kc_i8(As, ra);
+    else store_kc<VEC>(As, ra, p.K);
+    store_q_kc<GRP>(Bs, rb);
+  }
+};
+
+template <bool ACT, bool GRP, bool VEC>
+struct Loader<kDx, ACT, GRP, VEC> {
+  RegsKc ra;
+  RegsQKs rb;
+  __device__ __forceinline__ void load(const GemmArgs& p, int64_t m0, int64_t n0, int64_t k0) {
+    load_kc_bf16<VEC>(ra, static_cast<const uint16_t*>(p.a), p.lda, m0, p.M, k0, p.K);
+    load_q_ks<GRP>(rb, p, n0, k0);
+  }
+  __device__ __forceinline__ void store(const GemmArgs& p, uint16_t* As, uint16_t* Bs) {
+    store_kc<VEC>(As, ra, p.K);
+    store_q_ks(Bs, rb);
+  }
+};
+
+template <bool ACT, bool GRP, bool VEC>
+struct Loader<kDw, ACT, GRP, VEC> {
+  RegsKs ra;
+  typename std::conditional<ACT, RegsKs8, RegsKs>::type rb;
+  __device__ __forceinline__ void load(const GemmArgs& p, int64_t m0, int64_t n0, int64_t k0) {
+    load_ks_bf16<VEC>(ra, static_cast<const uint16_t*>(p.a), p.lda, m0, k0, p.K);
+    if constexpr (ACT) load_ks_i8(rb, static_cast<const int8_t*>(p.b), p.ldb, p.sx, n0, k0, p.K);
+    else load_ks_bf16<VEC>(rb, static_cast<const uint16_t*>(p.b), p.ldb, n0, k0, p.K);
+  }
+  __device__ __forceinline__ void store(const GemmArgs&, uint16_t* As, uint16_t* Bs) {
+    store_ks_bf16(As, ra);
+    if constexpr (ACT) store_ks_i8(Bs, rb);
+    else store_ks_bf16(Bs, rb);
+  }
+};
+
+// Offset of G[i][j] in the 256 x 256 bfloat16 staging tile of the dW epilogue
+// (16-byte chunks of a 512-byte row permuted by i mod 16).
+__device__ __forceinline__ int g_off(int i, int j) { return i * 256 + ((((j >> 3) ^ (i & 15))) << 3) + (j & 7); }
+
+// Instruction interleave of one K-tile (one scheduling region): the first
+// k-step's fragment reads, then each MFMA followed by a few VALU ops of the
+// next tile's conversion; the fragment reads of the following k-step ride on
+// the first MFMAs of each k-step, the LDS writes of the next tile and the
+// global loads of the tile after it are spread over the whole sequence.
+enum : int { SG_VALU = 0x2, SG_MFMA = 0x8, SG_VMEM_READ = 0x20, SG_DS_READ = 0x100, SG_DS_WRITE = 0x200 };
+
+__device__ __forceinline__ void interleave() {
+  __builtin_amdgcn_sched_group_barrier(SG_DS_READ, 8, 0);
+#pragma unroll
+  for (int m = 0; m < 64; ++m) {
+    __builtin_amdgcn_sched_group_barrier(SG_MFMA, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(SG_VALU, 3, 0);
+    if ((m & 15) < 8 && m < 48) __builtin_amdgcn_sched_group_barrier(SG_DS_READ, 1, 0);
+    if ((m & 3) == 3) __builtin_amdgcn_sched_group_barrier(SG_DS_WRITE, 1, 0);
+    if ((m & 3) == 1) __builtin_amdgcn_sched_group_barrier(SG_VMEM_READ, 1, 0);
+  }
+}
+
+template <int V, bool ACT, bool GRP, bool VEC>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void k_gemm(GemmArgs p) {
+  // A stages 0, 1 then B stages 0, 1 (128 KiB); the dW epilogue reuses all
+  // of it for G.
+  __shared__ __attribute__((aligned(16))) uint16_t lds[4 * TILE];
+  __shared__ float s_tile[256];                                     // dW epilogue: per-channel scales
+  __shared__ __attribute__((aligned(16))) uint16_t bt_tile[32 * 256];  // dW epilogue: B block (bf16)
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int64_t ntm = (p.M + BM - 1) / BM;
+  const int64_t tm = blockIdx.x % ntm, tn = blockIdx.x / ntm;
+  const int64_t m0 = tm * BM, n0 = tn * BN;
+  const int wm = (wave >> 1) * 128, wn = (wave & 1) * 128;
+
+  f32x16 acc[4][4];
+  #pragma unroll
+  for (int a = 0; a < 4; ++a)
+    #pragma unroll
+    for (int b = 0; b < 4; ++b)
+      #pragma unroll
+      for (int v = 0; v < 16; ++v) acc[a][b][v] = 0.f;
+
+  // Two register sets: while the MFMAs consume LDS stage kt%2, the tile
+  // kt+1 held in one set is written to the other stage and the tile kt+2
+  // is fetched into the other set.  Loads past the last tile read zeros or
+  // unused data and are never consumed, so the body has no branches.
+  Loader<V, ACT, GRP, VEC> L0, L1;
+  const int nk = int((p.K + BK - 1) / BK);
+  L0.load(p, m0, n0, 0);
+  L1.load(p, m0, n0, BK);
+  L0.store(p, lds, lds + 2 * TILE);
+  __syncthreads();
+
+  auto step = [&](int kt, Loader<V, ACT, GRP, VEC>& Lnext, Loader<V, ACT, GRP, VEC>& Lfree) {
+    const uint16_t* As = lds + (kt & 1) * TILE;
+    const uint16_t* Bs = lds + (2 + (kt & 1)) * TILE;
+    const int nx = (kt + 1) & 1;
+    Lfree.load(p, m0, n0, int64_t(kt + 2) * BK);
+    u32x4 fa[2][4], fb[2][4];
+    auto read = [&](u32x4 (&a)[4], u32x4 (&b)[4], int s) {
+      const int ch = 2 * s + (lane >> 5);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) a[i] = *reinterpret_cast<const u32x4*>(As + tile_off(wm + 32 * i + (lane & 31), ch));
+#pragma unroll
+      for (int j = 0; j < 4; ++j) b[j] = *reinterpret_cast<const u32x4*>(Bs + tile_off(wn + 32 * j + (lane & 31), ch));
+    };
+    read(fa[0], fb[0], 0);
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      if (s < 3) read(fa[(s + 1) & 1], fb[(s + 1) & 1], s + 1);
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          // forward / dX: D = B-tile x A-tile^T, so a lane's accumulator holds 4
+          // consecutive output columns of one output row (8-byte stores)
+          if constexpr (V == kDw) acc[i][j] = mfma32(fa[s & 1][i], fb[s & 1][j], acc[i][j]);
+          else acc[i][j] = mfma32(fb[s & 1][j], fa[s & 1][i], acc[i][j]);
+        }
+    }
+    Lnext.store(p, lds + nx * TILE, lds + (2 + nx) * TILE);
+    interleave();
+    __syncthreads();
+  };
+  int kt = 0;
+  for (; kt + 1 < nk; kt += 2) {
+    step(kt, L1, L0);
+    step(kt + 1, L0, L1);
+  }
+  if (kt < nk) step(kt, L1, L0);
+
+  if constexpr (V == kFwd || V == kDx) {
+    // acc[i][j][4g + e] = C[m0 + wm + 32 i + lane % 32][n0 + wn + 32 j + 8 g + 4 (lane / 32) + e]
+    uint16_t* out = static_cast<uint16_t*>(p.out);
+    const int64_t row_l = m0 + wm + (lane & 31);
+    const int64_t col_l = n0 + wn + 4 * (lane >> 5);
+    f32x4 cs[4][4];  // per-channel forward scales of the lane's columns
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int64_t c = col_l + 32 * j + 8 * g;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) cs[j][g][e] = (V == kFwd && !GRP && c + e < p.N) ? p.s[c + e] : 1.f;
+      }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int64_t row = row_l + 32 * i;
+      const float rs = (V == kFwd && ACT && row < p.M) ? p.sx[row] : 1.f;
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int64_t c = col_l + 32 * j + 8 * g;
+          float val[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) val[e] = acc[i][j][4 * g + e] * cs[j][g][e] * rs;
+          if (row < p.M) {
+            uint16_t* dst = out + row * p.ldo + c;
+            if (c + 4 <= p.N && (p.ldo & 3) == 0) {
+              *reinterpret_cast<u32x2*>(dst) = u32x2{pack_bf16x2(val[0], val[1]), pack_bf16x2(val[2], val[3])};
+            } else {
+#pragma unroll
+              for (int e = 0; e < 4; ++e)
+                if (c + e < p.N) dst[e] = __builtin_bit_cast(uint16_t, (__bf16)val[e]);
+            }
+          }
+        }
+    }
+  } else {
+    // ---- dW epilogue: G = s * M * dW, then the rank-r products.
+    // Accumulator layout: acc[i][j][v] = dW[m0 + wm + 32 i + acc_row(v)][n0 + wn + 32 j + lane % 32].
+    // LDS: G (bf16, 128 KiB) in `lds`, the B block of the current rank block
+    // (bf16 [32][256]) in `bt_tile`, per-channel scales in `s_tile`.
+    const int r = p.r;
+    const int nrb = (r + 31) / 32;
+    const int half = lane >> 5;
+    const int64_t rowb = m0 + wm;  // first row of the wave
+
+    // B[32 rb + rho][n0 .. n0 + 255] as bf16; thread t converts 32 values of row t / 8
+    auto stage_b = [&](int rb) {
+      const int rho = 32 * rb + (threadIdx.x >> 3), c0 = 32 * (threadIdx.x & 7);
+      const bool ok = rho < r;
+      const bool bvec = (p.N % 4 == 0) && (reinterpret_cast<uintptr_t>(p.Bm) & 15) == 0;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int64_t col = n0 + c0 + 8 * q;
+        float x[8];
+        if (ok && bvec && col + 8 <= p.N) {
+          const f32x4 u = *reinterpret_cast<const f32x4*>(p.Bm + int64_t(rho) * p.N + col);
+          const f32x4 w = *reinterpret_cast<const f32x4*>(p.Bm + int64_t(rho) * p.N + col + 4);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            x[e] = u[e];
+            x[4 + e] = w[e];
+          }
+        } else {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) x[e] = (ok && col + e < p.N) ? p.Bm[int64_t(rho) * p.N + col + e] : 0.f;
+        }
+        u32x4 o;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) o[e] = pack_bf16x2(x[2 * e], x[2 * e + 1]);
+        *reinterpret_cast<u32x4*>(&bt_tile[(threadIdx.x >> 3) * 256 + c0 + 8 * q]) = o;
+      }
+    };
+    // A operand of the dB product: rows rowb + 32 i + acc_row(8 s2 + e), the lane's accumulator rows
+    auto load_aop = [&](u32x4 (&aop)[4][2], int rb) {
+      const int rho = 32 * rb + (lane & 31);
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int s2 = 0; s2 < 2; ++s2) {
+          float x[8];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const int64_t row = rowb + 32 * i + acc_row(8 * s2 + e, lane);
+            x[e] = (rho < r && row < p.M) ? p.Am[row * r + rho] : 0.f;
+          }
+#pragma unroll
+          for (int q = 0; q < 4; ++q) aop[i][s2][q] = pack_bf16x2(x[2 * q], x[2 * q + 1]);
+        }
+    };
+
+    // one round of loads: mask bits, scales, the first B block and A operand
+    u32x4 mbits[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int64_t col = n0 + wn + 32 * j + (lane & 31);
+      mbits[j] = u32x4{0u, 0u, 0u, 0u};
+      if (col < p.N) mbits[j] = *reinterpret_cast<const u32x4*>(p.mask + col * p.ldm + (rowb >> 3));
+    }
+    if constexpr (!GRP) {
+      const int64_t row = m0 + threadIdx.x;
+      s_tile[threadIdx.x] = row < p.M ? p.s[row] : 0.f;
+    }
+    stage_b(0);
+    u32x4 aop[4][2];
+    load_aop(aop, 0);
+    __syncthreads();  // scales and the first B block staged
+
+    uint16_t* Gs = lds;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int g4 = 0; g4 < 4; ++g4) {
+        // scales of the 4 consecutive rows 32 i + 8 g4 + 4 half .. +3 of the wave
+        const int lr = wm + 32 * i + 8 * g4 + 4 * half;
+        f32x4 sc4 = {0.f, 0.f, 0.f, 0.f};
+        if constexpr (!GRP) sc4 = *reinterpret_cast<const f32x4*>(&s_tile[lr]);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int lj = wn + 32 * j + (lane & 31);
+          const int64_t col = n0 + lj;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int v = 4 * g4 + e;
+            const int li = lr + e;
+            // the padded mask region past row m is not written by the grid pass
+            const bool in = (mbits[j][i] >> acc_row(v, lane)) & 1 && m0 + li < p.M && col < p.N;
+            float sc;
+            if constexpr (GRP) sc = in ? p.s[(m0 + li) * p.ngroups + col / p.gsize] : 0.f;
+            else sc = sc4[e];
+            const float g = in ? acc[i][j][v] * sc : 0.f;
+            acc[i][j][v] = g;
+            Gs[g_off(li, lj)] = __builtin_bit_cast(uint16_t, (__bf16)g);
+          }
+        }
+      }
+
+    // ---- dB partial [2 tm + wave row][rho][col] = sum_i A[m0 + i][rho] G[i][col]  (G from registers)
+    const int64_t part = 2 * tm + (wave >> 1);
+    for (int rb = 0; rb < nrb; ++rb) {
+      if (rb > 0) load_aop(aop, rb);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        f32x16 d;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) d[v] = 0.f;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int s2 = 0; s2 < 2; ++s2) {
+            u32x4 gop;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) gop[q] = pack_bf16x2(acc[i][j][8 * s2 + 2 * q], acc[i][j][8 * s2 + 2 * q + 1]);
+            d = mfma32(aop[i][s2], gop, d);
+          }
+        const int64_t col = n0 + wn + 32 * j + (lane & 31);
+        if (col < p.N) {
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            const int rr = 32 * rb + acc_row(v, lane);
+            if (rr < r) p.dB_part[(part * r + rr) * p.N + col] = d[v];
+          }
+        }
+      }
+    }
+    __syncthreads();  // G staged
+
+    // ---- dA partial [tn][row][rho] = sum_j G[row][j] B[rho][n0 + j]   (both operands from LDS)
+    for (int rb = 0; rb < nrb; ++rb) {
+      if (rb > 0) {
+        __syncthreads();  // every wave is done with the previous B block
+        stage_b(rb);
+        __syncthreads();
+      }
+      const int rho = 32 * rb + (lane & 31);
+#pragma unroll
+      for (int h2 = 0; h2 < 2; ++h2) {
+        const int rowblk = 2 * wave + h2;
+        f32x16 d;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) d[v] = 0.f;
+#pragma unroll
+        for (int s2 = 0; s2 < 16; ++s2) {
+          const int li = 32 * rowblk + (lane & 31);
+          const u32x4 ga = *reinterpret_cast<const u32x4*>(Gs + g_off(li, 16 * s2 + 8 * half));
+          const u32x4 bb = *reinterpret_cast<const u32x4*>(&bt_tile[(lane & 31) * 256 + 16 * s2 + 8 * half]);
+          d = mfma32(ga, bb, d);
+        }
+        if (rho < r) {
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            const int64_t row = m0 + 32 * rowblk + acc_row(v, lane);
+            if (row < p.M) p.dA_part[(tn * p.M + row) * r + rho] = d[v];
+          }
+        }
+      }
+    }
+  }
+}
+
+// Launch one instantiation (all variants share this helper).
+template <int V, bool ACT, bool GRP>
+hipError_t launch_variant(const GemmArgs& p, hipStream_t st) {
+  const int64_t ntm = (p.M + BM - 1) / BM, ntn = (p.N + BN - 1) / BN;
+  // fast path: 16-byte row vectors (leading dimensions multiples of 8
+  // elements) and, for K-contiguous operands, no partial last K-tile
+  const bool vec = (p.lda % 8 == 0) && (V != kDw || p.ldb % 8 == 0) && (V == kDw || p.K % BK == 0);
+  if (vec) k_gemm<V, ACT, GRP, true><<<unsigned(ntm * ntn), 256, 0, st>>>(p);
+  else k_gemm<V, ACT, GRP, false><<<unsigned(ntm * ntn), 256, 0, st>>>(p);
+  return hipGetLastError();
+}
+
+}  // namespace lrqat

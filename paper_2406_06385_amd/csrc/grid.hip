@@ -226,16 +226,16 @@ __global__ __launch_bounds__(256) void k_grid(GridArgs a) {
       }
     }
   }
-  // Clip-mask bits: bit (col % 8) of byte col / 8; 32 columns per thread.
+  // Clip-mask bits, transposed: bit (row % 8) of byte [col][row / 8]; one
+  // 32-row word per thread (column t % 128, rows 32 (t / 128) .. +31).
   if (a.mout) {
-    const int lr = threadIdx.x >> 2, seg = threadIdx.x & 3;
-    const int64_t row = row0 + lr;
-    const int64_t cbase = col0 + 32 * seg;
-    if (row < a.m && cbase < a.kq) {
+    const int c = threadIdx.x & 127, hr = threadIdx.x >> 7;
+    const int64_t col = col0 + c;
+    if (col < a.kq) {
       uint32_t bitsw = 0;
-      #pragma unroll
-      for (int e = 0; e < 32; ++e) bitsw |= uint32_t((qs[lr][32 * seg + e] >> 4) & 1) << e;
-      *reinterpret_cast<uint32_t*>(a.mout + row * a.ldm + (cbase >> 3)) = bitsw;
+#pragma unroll
+      for (int e = 0; e < 32; ++e) bitsw |= uint32_t((qs[32 * hr + e][c] >> 4) & 1) << e;
+      *reinterpret_cast<uint32_t*>(a.mout + col * a.ldm + ((row0 + 32 * hr) >> 3)) = bitsw;
     }
   }
 }

@@ -20,8 +20,8 @@ struct GridArgs {
   uint8_t* qout;         // packed q [m][ldq]
   int64_t ldq;           // bytes per row of qout
   int64_t kq;            // columns written per row of qout (>= k; columns >= k are 0)
-  uint8_t* mout;         // clip-mask bits [m][ldm] (nullable)
-  int64_t ldm;           // bytes per row of mout
+  uint8_t* mout;         // clip-mask bits, transposed: bit (row % 8) of byte [col][row / 8] (nullable)
+  int64_t ldm;           // bytes per column of mout (rows padded to a multiple of 256)
 };
 
 // bf16 MFMA GEMM family.  C[M][N] = sum_K a(M, K) b(K, N) with the operand
@@ -39,7 +39,7 @@ struct GemmArgs {
   const float* sx;        // per-token activation scale [T] (W4A8) or null
   void* out;              // kFwd: Y [T][m]; kDx: dX [T][k]
   int64_t ldo;
-  const uint8_t* mask;    // kDw: clip-mask bits [m][ldm]
+  const uint8_t* mask;    // kDw: transposed clip-mask bits [k][ldm]
   int64_t ldm;
   const float* Am;        // kDw: A [m][r]
   const float* Bm;        // kDw: B [r][k]
@@ -58,6 +58,17 @@ hipError_t launch_grid(const GridArgs& a, hipStream_t st);
 hipError_t launch_act_quant(const uint16_t* X, int64_t T, int64_t k, int8_t* n, int64_t ldn, float* sx,
                             hipStream_t st);
 hipError_t launch_gemm(GemmVariant v, bool act, bool grouped, const GemmArgs& p, hipStream_t st);
+// per-variant launchers (gemm_fwd.hip, gemm_fwd_act.hip, gemm_dx.hip, gemm_dw.hip, gemm_dw_act.hip)
+hipError_t launch_fwd(const GemmArgs& p, hipStream_t st);
+hipError_t launch_fwd_grp(const GemmArgs& p, hipStream_t st);
+hipError_t launch_fwd_act(const GemmArgs& p, hipStream_t st);
+hipError_t launch_fwd_act_grp(const GemmArgs& p, hipStream_t st);
+hipError_t launch_dx(const GemmArgs& p, hipStream_t st);
+hipError_t launch_dx_grp(const GemmArgs& p, hipStream_t st);
+hipError_t launch_dw(const GemmArgs& p, hipStream_t st);
+hipError_t launch_dw_grp(const GemmArgs& p, hipStream_t st);
+hipError_t launch_dw_act(const GemmArgs& p, hipStream_t st);
+hipError_t launch_dw_act_grp(const GemmArgs& p, hipStream_t st);
 hipError_t launch_reduce(const float* part, int64_t nparts, int64_t n, float* out, float c, int accumulate,
                          hipStream_t st);
 
@@ -70,7 +81,7 @@ struct F32Args {
   const float* dY;
   const uint8_t* q;       // packed q [m][ldq]
   int64_t ldq;
-  const uint8_t* mask;    // [m][ldm]
+  const uint8_t* mask;    // transposed clip-mask bits [k][ldm]
   int64_t ldm;
   const float* s;
   int64_t gsize, ngroups;
