@@ -144,7 +144,7 @@ Workspace layout(const Dims& d, int64_t T, bool backward) {
     if (d.bf16) {
       const int64_t ntn = (d.k + GEMM_BN - 1) / GEMM_BN, ntm = (d.m + GEMM_BM - 1) / GEMM_BM;
       w.dA_part = take(size_t(ntn * d.m * d.r * 4));
-      w.dB_part = take(size_t(2 * ntm * d.r * d.k * 4));
+      w.dB_part = take(size_t(ntm * d.r * d.k * 4));
     } else {
       w.G = take(size_t(d.m * d.k * 4));
     }
@@ -363,7 +363,7 @@ lrqat_status lrqat_backward(const lrqat_layer* layer, int64_t tokens, const void
   const int64_t ntn = (d.k + GEMM_BN - 1) / GEMM_BN, ntm = (d.m + GEMM_BM - 1) / GEMM_BM;
   LRQAT_TRY(hip_status(timed("reduce", st, [&] { return launch_reduce(dA_part, ntn, d.m * d.r, dA, d.c, accumulate, st); }),
                        "reduce"));
-  LRQAT_TRY(hip_status(timed("reduce", st, [&] { return launch_reduce(dB_part, 2 * ntm, d.r * d.k, dB, d.c, accumulate, st); }),
+  LRQAT_TRY(hip_status(timed("reduce", st, [&] { return launch_reduce(dB_part, ntm, d.r * d.k, dB, d.c, accumulate, st); }),
                        "reduce"));
   return LRQAT_OK;
 }

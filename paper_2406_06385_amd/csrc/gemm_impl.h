@@ -210,9 +210,14 @@ __device__ __forceinline__ void load_q_ks(RegsQKs& R, const GemmArgs& p, int64_t
 #pragma unroll
     for (int e = 0; e < 8; ++e) R.sc[e] = ldf(rs, sb + e * sstep);
   } else {
+    // the 8 rows' scales are consecutive: two 16-byte loads (rows past K read as zeros)
     const auto rs = rsrc(p.s + k0, (p.K - k0) * 4);
+    const u32x4 s0 = ld128(rs, uint32_t(8 * kg * 4)), s1 = ld128(rs, uint32_t((8 * kg + 4) * 4));
 #pragma unroll
-    for (int e = 0; e < 8; ++e) R.sc[e] = ldf(rs, uint32_t((8 * kg + e) * 4));
+    for (int e = 0; e < 4; ++e) {
+      R.sc[e] = __uint_as_float(s0[e]);
+      R.sc[4 + e] = __uint_as_float(s1[e]);
+    }
   }
 }
 
@@ -346,9 +351,11 @@ struct Loader<kDw, ACT, GRP, VEC> {
   }
 };
 
-// Offset of G[i][j] in the 256 x 256 bfloat16 staging tile of the dW epilogue
-// (16-byte chunks of a 512-byte row permuted by i mod 16).
-__device__ __forceinline__ int g_off(int i, int j) { return i * 256 + ((((j >> 3) ^ (i & 15))) << 3) + (j & 7); }
+// Offset of element (i, j) in a [rows][256] bfloat16 staging tile of the dW
+// epilogue (G, and the B block): the 32 16-byte chunks of a 512-byte row are
+// permuted by i mod 32, so 32 consecutive rows read at one column hit 32
+// different chunk slots.
+__device__ __forceinline__ int g_off(int i, int j) { return i * 256 + ((((j >> 3) ^ (i & 31))) << 3) + (j & 7); }
 
 // Instruction interleave of one K-tile (one scheduling region): the first
 // k-step's fragment reads, then each MFMA followed by a few VALU ops of the
@@ -369,16 +376,35 @@ __device__ __forceinline__ void interleave() {
   }
 }
 
+// Block -> tile order.  Blocks are dealt round-robin to the 8 XCDs (each with
+// its own L2), so block b is renumbered to v = (b % 8) * (nt / 8) + b / 8: the
+// blocks an XCD runs get consecutive numbers.  v then walks the tiles in
+// groups of 4 tile rows (all columns of a group before the next group), so an
+// XCD's concurrent blocks cover a compact 4 x 8 patch of tiles and share
+// operand strips in its L2.
+__device__ __forceinline__ void tile_of(int64_t b, int64_t ntm, int64_t ntn, int64_t& tm, int64_t& tn) {
+  const int64_t nt = ntm * ntn, per = nt / 8;
+  const int64_t v = b < per * 8 ? (b % 8) * per + b / 8 : b;
+  constexpr int64_t GM = 4;
+  const int64_t gsz = GM * ntn;
+  const int64_t first = (v / gsz) * GM;
+  const int64_t gm = ntm - first < GM ? ntm - first : GM;
+  const int64_t off = v % gsz;
+  tm = first + off % gm;
+  tn = off / gm;
+}
+
 template <int V, bool ACT, bool GRP, bool VEC>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void k_gemm(GemmArgs p) {
   // A stages 0, 1 then B stages 0, 1 (128 KiB); the dW epilogue reuses all
   // of it for G.
   __shared__ __attribute__((aligned(16))) uint16_t lds[4 * TILE];
   __shared__ float s_tile[256];                                     // dW epilogue: per-channel scales
-  __shared__ __attribute__((aligned(16))) uint16_t bt_tile[32 * 256];  // dW epilogue: B block (bf16)
+  __shared__ __attribute__((aligned(16))) uint16_t rt_tile[32 * 256];  // dW epilogue: A or B rank block (bf16)
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int64_t ntm = (p.M + BM - 1) / BM;
-  const int64_t tm = blockIdx.x % ntm, tn = blockIdx.x / ntm;
+  int64_t tm, tn;
+  tile_of(int64_t(blockIdx.x), ntm, (p.N + BN - 1) / BN, tm, tn);
   const int64_t m0 = tm * BM, n0 = tn * BN;
   const int wm = (wave >> 1) * 128, wn = (wave & 1) * 128;
 
@@ -478,61 +504,16 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
         }
     }
   } else {
-    // ---- dW epilogue: G = s * M * dW, then the rank-r products.
+    // ---- dW epilogue: G = s * M * dW staged in LDS (bf16), then both rank-r
+    // products from LDS; the accumulators are dead once G is staged.
     // Accumulator layout: acc[i][j][v] = dW[m0 + wm + 32 i + acc_row(v)][n0 + wn + 32 j + lane % 32].
-    // LDS: G (bf16, 128 KiB) in `lds`, the B block of the current rank block
-    // (bf16 [32][256]) in `bt_tile`, per-channel scales in `s_tile`.
     const int r = p.r;
     const int nrb = (r + 31) / 32;
     const int half = lane >> 5;
     const int64_t rowb = m0 + wm;  // first row of the wave
+    uint16_t* Gs = lds;
 
-    // B[32 rb + rho][n0 .. n0 + 255] as bf16; thread t converts 32 values of row t / 8
-    auto stage_b = [&](int rb) {
-      const int rho = 32 * rb + (threadIdx.x >> 3), c0 = 32 * (threadIdx.x & 7);
-      const bool ok = rho < r;
-      const bool bvec = (p.N % 4 == 0) && (reinterpret_cast<uintptr_t>(p.Bm) & 15) == 0;
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int64_t col = n0 + c0 + 8 * q;
-        float x[8];
-        if (ok && bvec && col + 8 <= p.N) {
-          const f32x4 u = *reinterpret_cast<const f32x4*>(p.Bm + int64_t(rho) * p.N + col);
-          const f32x4 w = *reinterpret_cast<const f32x4*>(p.Bm + int64_t(rho) * p.N + col + 4);
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            x[e] = u[e];
-            x[4 + e] = w[e];
-          }
-        } else {
-#pragma unroll
-          for (int e = 0; e < 8; ++e) x[e] = (ok && col + e < p.N) ? p.Bm[int64_t(rho) * p.N + col + e] : 0.f;
-        }
-        u32x4 o;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) o[e] = pack_bf16x2(x[2 * e], x[2 * e + 1]);
-        *reinterpret_cast<u32x4*>(&bt_tile[(threadIdx.x >> 3) * 256 + c0 + 8 * q]) = o;
-      }
-    };
-    // A operand of the dB product: rows rowb + 32 i + acc_row(8 s2 + e), the lane's accumulator rows
-    auto load_aop = [&](u32x4 (&aop)[4][2], int rb) {
-      const int rho = 32 * rb + (lane & 31);
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int s2 = 0; s2 < 2; ++s2) {
-          float x[8];
-#pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            const int64_t row = rowb + 32 * i + acc_row(8 * s2 + e, lane);
-            x[e] = (rho < r && row < p.M) ? p.Am[row * r + rho] : 0.f;
-          }
-#pragma unroll
-          for (int q = 0; q < 4; ++q) aop[i][s2][q] = pack_bf16x2(x[2 * q], x[2 * q + 1]);
-        }
-    };
-
-    // one round of loads: mask bits, scales, the first B block and A operand
+    // clip-mask bits of the lane's four columns over the wave's 128 rows (transposed layout)
     u32x4 mbits[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
@@ -543,13 +524,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     if constexpr (!GRP) {
       const int64_t row = m0 + threadIdx.x;
       s_tile[threadIdx.x] = row < p.M ? p.s[row] : 0.f;
+      __syncthreads();
     }
-    stage_b(0);
-    u32x4 aop[4][2];
-    load_aop(aop, 0);
-    __syncthreads();  // scales and the first B block staged
-
-    uint16_t* Gs = lds;
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -572,68 +548,88 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
             if constexpr (GRP) sc = in ? p.s[(m0 + li) * p.ngroups + col / p.gsize] : 0.f;
             else sc = sc4[e];
             const float g = in ? acc[i][j][v] * sc : 0.f;
-            acc[i][j][v] = g;
             Gs[g_off(li, lj)] = __builtin_bit_cast(uint16_t, (__bf16)g);
           }
         }
       }
 
-    // ---- dB partial [2 tm + wave row][rho][col] = sum_i A[m0 + i][rho] G[i][col]  (G from registers)
-    const int64_t part = 2 * tm + (wave >> 1);
-    for (int rb = 0; rb < nrb; ++rb) {
-      if (rb > 0) load_aop(aop, rb);
+    // stage rank block rb of A (transposed) or B as bf16 [32][256] in `rt_tile`
+    auto stage = [&](const float* __restrict__ src, bool is_a, int rb) {
+      const int rho_l = threadIdx.x >> 3, c0 = 32 * (threadIdx.x & 7);
+      const int rho = 32 * rb + rho_l;
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
+      for (int q = 0; q < 4; ++q) {
+        float x[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const int c = c0 + 8 * q + e;
+          if (is_a) x[e] = (rho < r && m0 + c < p.M) ? src[(m0 + c) * r + rho] : 0.f;   // A[m0 + c][rho]
+          else x[e] = (rho < r && n0 + c < p.N) ? src[int64_t(rho) * p.N + n0 + c] : 0.f;  // B[rho][n0 + c]
+        }
+        u32x4 o;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) o[e] = pack_bf16x2(x[2 * e], x[2 * e + 1]);
+        *reinterpret_cast<u32x4*>(&rt_tile[g_off(rho_l, c0 + 8 * q)]) = o;
+      }
+    };
+
+    // dB partial [tm][rho][n0 + j] = sum_i A[m0 + i][rho] G[i][j]; dA partial [tn][m0 + i][rho] = sum_j G[i][j] B[rho][n0 + j]
+    const auto rdb = rsrc(p.dB_part + tm * r * p.N + n0, (int64_t(r) * p.N - n0) * 4);
+    const auto rda = rsrc(p.dA_part + (tn * p.M + m0) * r, (p.M - m0) * int64_t(r) * 4);
+    for (int rb = 0; rb < nrb; ++rb) {
+      const int rho = 32 * rb + (lane & 31);
+      __syncthreads();  // G staged / previous rank block consumed
+      stage(p.Am, true, rb);
+      __syncthreads();
+      // dB: A operand = A^T rows (rt_tile), B operand = 8 consecutive rows of a G column
+#pragma unroll
+      for (int cb2 = 0; cb2 < 2; ++cb2) {
+        const int cb = 2 * wave + cb2;            // column block of 32
+        const int lj = 32 * cb + (lane & 31);
         f32x16 d;
 #pragma unroll
         for (int v = 0; v < 16; ++v) d[v] = 0.f;
+#pragma unroll 4
+        for (int s2 = 0; s2 < 16; ++s2) {
+          const int ib = 16 * s2 + 8 * half;
+          const u32x4 aa = *reinterpret_cast<const u32x4*>(&rt_tile[g_off(lane & 31, ib)]);
+          u32x4 gb;
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-          for (int s2 = 0; s2 < 2; ++s2) {
-            u32x4 gop;
-#pragma unroll
-            for (int q = 0; q < 4; ++q) gop[q] = pack_bf16x2(acc[i][j][8 * s2 + 2 * q], acc[i][j][8 * s2 + 2 * q + 1]);
-            d = mfma32(aop[i][s2], gop, d);
-          }
-        const int64_t col = n0 + wn + 32 * j + (lane & 31);
-        if (col < p.N) {
+          for (int q = 0; q < 4; ++q)
+            gb[q] = uint32_t(Gs[g_off(ib + 2 * q, lj)]) | (uint32_t(Gs[g_off(ib + 2 * q + 1, lj)]) << 16);
+          d = mfma32(aa, gb, d);
+        }
+        if (n0 + lj < p.N) {
 #pragma unroll
           for (int v = 0; v < 16; ++v) {
             const int rr = 32 * rb + acc_row(v, lane);
-            if (rr < r) p.dB_part[(part * r + rr) * p.N + col] = d[v];
+            if (rr < r)
+              __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(d[v]), rdb, int(uint32_t((int64_t(rr) * p.N + lj) * 4)), 0, 0);
           }
         }
       }
-    }
-    __syncthreads();  // G staged
-
-    // ---- dA partial [tn][row][rho] = sum_j G[row][j] B[rho][n0 + j]   (both operands from LDS)
-    for (int rb = 0; rb < nrb; ++rb) {
-      if (rb > 0) {
-        __syncthreads();  // every wave is done with the previous B block
-        stage_b(rb);
-        __syncthreads();
-      }
-      const int rho = 32 * rb + (lane & 31);
+      __syncthreads();
+      stage(p.Bm, false, rb);
+      __syncthreads();
+      // dA: A operand = G rows, B operand = B rows (rt_tile)
 #pragma unroll
       for (int h2 = 0; h2 < 2; ++h2) {
         const int rowblk = 2 * wave + h2;
         f32x16 d;
 #pragma unroll
         for (int v = 0; v < 16; ++v) d[v] = 0.f;
-#pragma unroll
+#pragma unroll 4
         for (int s2 = 0; s2 < 16; ++s2) {
           const int li = 32 * rowblk + (lane & 31);
           const u32x4 ga = *reinterpret_cast<const u32x4*>(Gs + g_off(li, 16 * s2 + 8 * half));
-          const u32x4 bb = *reinterpret_cast<const u32x4*>(&bt_tile[(lane & 31) * 256 + 16 * s2 + 8 * half]);
+          const u32x4 bb = *reinterpret_cast<const u32x4*>(&rt_tile[g_off(lane & 31, 16 * s2 + 8 * half)]);
           d = mfma32(ga, bb, d);
         }
         if (rho < r) {
 #pragma unroll
           for (int v = 0; v < 16; ++v) {
-            const int64_t row = m0 + 32 * rowblk + acc_row(v, lane);
-            if (row < p.M) p.dA_part[(tn * p.M + row) * r + rho] = d[v];
+            const int row = 32 * rowblk + acc_row(v, lane);
+            __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(d[v]), rda, int(uint32_t((row * r + rho) * 4)), 0, 0);
           }
         }
       }

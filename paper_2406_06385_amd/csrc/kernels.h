@@ -45,7 +45,7 @@ struct GemmArgs {
   const float* Bm;        // kDw: B [r][k]
   int r;
   float* dA_part;         // kDw: [ceil(N/256)][M][r]
-  float* dB_part;         // kDw: [2*ceil(M/256)][r][N]
+  float* dB_part;         // kDw: [ceil(M/256)][r][N]
 };
 
 constexpr int GEMM_BM = 256, GEMM_BN = 256, GEMM_BK = 64;
