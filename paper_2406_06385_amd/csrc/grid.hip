@@ -58,15 +58,24 @@ __global__ __launch_bounds__(256) void k_encode(const float* __restrict__ W0, co
 }
 
 // ============================================================================ grid
-// Tile 64 rows x 128 columns per block of 4 waves; wave w covers rows
-// 32*(w/2) and columns 64*(w%2) as two 32x32 MFMA blocks.  delta = c A B is
-// an MFMA product of bfloat16 hi/lo splits, A B ~ Ahi Bhi + Ahi Blo + Alo Bhi,
+// Tile 64 rows x 128 columns per block of 8 waves; wave w covers the 32x32
+// block at rows 32*(w/4), columns 32*(w%4).  delta = c A B is an MFMA
+// product of bfloat16 hi/lo splits, A B ~ Ahi Bhi + Ahi Blo + Alo Bhi,
 // accumulated in float32.  Its error is below 3*2^-16 sum_rho |A||B| plus the
-// float32 accumulation, bounded here by 2^-13 |c| max_i ||A_i|| ||B_:j||
-// (Cauchy-Schwarz).  An element whose pre-round value lies within that bound
+// float32 accumulation, bounded here by 2^-13 |c| ||A_i|| max_j ||B_:j||
+// (Cauchy-Schwarz) <= 2^-13 |c| r max|A_i:| max|B_:j|.  An element whose pre-round value lies within that bound
 // of a rounding decision point is decided again from a float64 delta, so the
 // grid equals the exact one except within float64 rounding of a .5 point.
-constexpr int GR_BM = 64, GR_BN = 128;
+//
+// The product is formed transposed (B columns as the MFMA row operand), so a
+// lane owns one weight row and the columns 8 g + 4 (lane / 32) + e
+// (g, e = 0..3) of its wave's block: its Phi0 codes come as one 32-bit (Q8)
+// or 16-bit (packed) LDS read per 4 elements, its q nibbles pack in
+// registers, and the transposed clip mask is one wave ballot per column pair.
+// The pass is latency-bound (one short dependent chain per block), so the
+// per-lane state is kept small for occupancy.
+constexpr int GR_BM = 64, GR_BN = 128, GR_THREADS = 512;
+constexpr int GR_PITCH = 136;  // LDS bytes per staged Phi0 row: 34 dwords keeps the 32 rows of a read on distinct banks
 
 // 8 consecutive floats -> bf16 hi part and bf16 lo part (x - hi), packed.
 __device__ __forceinline__ void split8(const float (&x)[8], u32x4& hi, u32x4& lo) {
@@ -83,52 +92,44 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t grid_rsrc(const void* base, in
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), short(0), int(uint32_t(n)), 0x00020000);
 }
 
-__global__ __launch_bounds__(256) void k_grid(GridArgs a) {
-  __shared__ uint8_t qs[GR_BM][GR_BN];     // (q & 15) | 0x10 when the element is inside the grid
-  __shared__ uint8_t ph[GR_BM][GR_BN];     // the block's Phi0 bytes (GR_BN/2 per row when packed)
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int64_t ncb = (a.kq + GR_BN - 1) / GR_BN;
-  const int64_t row0 = int64_t(blockIdx.x / ncb) * GR_BM;
-  const int64_t col0 = int64_t(blockIdx.x % ncb) * GR_BN;
-  const int wr = 32 * (wave >> 1), wc = 64 * (wave & 1);
+// Phi0 code e (0..3) of a 32-bit word of four Q8 bytes or a 16-bit word of four packed nibbles.
+template <bool PACKED>
+__device__ __forceinline__ int code_of(uint32_t w, int e) {
+  if constexpr (PACKED) return int(w << (28 - 4 * e)) >> 28;
+  else return int(w << (24 - 8 * e)) >> 24;
+}
+
+template <bool PACKED>
+__device__ __forceinline__ uint32_t read_codes(const uint8_t* ph, int lr, int lc) {
+  if constexpr (PACKED) return *reinterpret_cast<const uint16_t*>(ph + lr * GR_PITCH + (lc >> 1));
+  else return *reinterpret_cast<const uint32_t*>(ph + lr * GR_PITCH + lc);
+}
+
+// Decision, packing and mask of one block after its Phi0 tile is staged
+// (the caller's barrier follows the rank-r product inside).
+template <bool PACKED, bool FULL>
+__device__ __forceinline__ void grid_body(const GridArgs& a, const uint8_t* ph, int64_t row0, int64_t col0) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, half = lane >> 5;
+  const int wr = 32 * (wave >> 2), wc = 32 * (wave & 3);
   const int lo = -(1 << (a.bits - 1)), hi = (1 << (a.bits - 1)) - 1;
-  const int f = a.packed ? 0 : 8 - a.bits;
+  const int f = PACKED ? 0 : 8 - a.bits;
 
-  // Stage the Phi0 tile in LDS first so its loads overlap the rank-r product.
-  // Rows past m read as zeros (buffer range); columns past k are never used.
-  {
-    const int64_t bpr = a.packed ? GR_BN / 2 : GR_BN;          // bytes per tile row
-    const int64_t cb0 = a.packed ? col0 / 2 : col0;
-    const auto r = grid_rsrc(a.phi0 + row0 * a.ld_phi + cb0, (a.m - row0) * a.ld_phi - cb0);
-    const int tr = threadIdx.x >> 2, seg = threadIdx.x & 3;   // 4 threads per row
-    const int64_t nbytes = bpr / 4;                            // 32 (fixed point) or 16 (packed)
-    if ((a.ld_phi & 15) == 0) {
-      for (int64_t o = 0; o < nbytes; o += 16) {
-        const u32x4 v = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
-            r, int(tr * a.ld_phi + seg * nbytes + o), 0, 0));
-        *reinterpret_cast<u32x4*>(&ph[tr][seg * nbytes + o]) = v;
-      }
-    } else {
-      for (int64_t o = 0; o < nbytes; ++o)
-        ph[tr][seg * nbytes + o] = uint8_t(__builtin_amdgcn_raw_buffer_load_b8(r, int(tr * a.ld_phi + seg * nbytes + o), 0, 0));
-    }
-  }
-
-  f32x16 acc[2];
+  // acc[v] = (A B)[row0 + wr + lane % 32][col0 + wc + acc_row(v, lane)]
+  f32x16 acc;
 #pragma unroll
-  for (int b = 0; b < 2; ++b)
-#pragma unroll
-    for (int v = 0; v < 16; ++v) acc[b][v] = 0.f;
+  for (int v = 0; v < 16; ++v) acc[v] = 0.f;
 
   const int64_t arow = row0 + wr + (lane & 31);
-  const int half = lane >> 5;
-  const bool avec = (a.r & 3) == 0 && (reinterpret_cast<uintptr_t>(a.A) & 15) == 0;
-  float a2 = 0.f, b2[2] = {0.f, 0.f};  // squared norms: the lane's A row, its B columns
+  const int64_t bcol = col0 + wc + (lane & 31);
+  const bool avec = FULL || ((a.r & 3) == 0 && (reinterpret_cast<uintptr_t>(a.A) & 15) == 0);
+  // max |A| over the lane's row and max |B| over its column: ||x|| <= sqrt(r) max|x| bounds the
+  // norms, and a zero maximum means an exactly zero delta
+  float amax = 0.f, bmax = 0.f;
   for (int r0 = 0; r0 < a.r; r0 += 16) {
-    // A operand: A[arow][r0 + 8*half + e]
-    float x[8];
+    // A operand: A[arow][r0 + 8*half + e]; B operand: B[r0 + 8*half + e][bcol]
+    float x[8], y[8];
     const int rb = r0 + 8 * half;
-    if (avec && arow < a.m && rb + 8 <= a.r) {
+    if (FULL || (avec && arow < a.m && rb + 8 <= a.r)) {
       const f32x4 u = *reinterpret_cast<const f32x4*>(a.A + arow * a.r + rb);
       const f32x4 w = *reinterpret_cast<const f32x4*>(a.A + arow * a.r + rb + 4);
 #pragma unroll
@@ -141,52 +142,60 @@ __global__ __launch_bounds__(256) void k_grid(GridArgs a) {
       for (int e = 0; e < 8; ++e) x[e] = (arow < a.m && rb + e < a.r) ? a.A[arow * a.r + rb + e] : 0.f;
     }
 #pragma unroll
-    for (int e = 0; e < 8; ++e) a2 += x[e] * x[e];
-    u32x4 ahi, alo;
-    split8(x, ahi, alo);
+    for (int e = 0; e < 8; ++e)
+      y[e] = (FULL || (bcol < a.k && rb + e < a.r)) ? a.B[int64_t(rb + e) * a.k + bcol] : 0.f;
 #pragma unroll
-    for (int b = 0; b < 2; ++b) {
-      const int64_t bcol = col0 + wc + 32 * b + (lane & 31);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        x[e] = (bcol < a.k && rb + e < a.r) ? a.B[int64_t(rb + e) * a.k + bcol] : 0.f;
-        b2[b] += x[e] * x[e];
-      }
-      u32x4 bhi, blo;
-      split8(x, bhi, blo);
-      acc[b] = mfma32(ahi, bhi, acc[b]);
-      acc[b] = mfma32(ahi, blo, acc[b]);
-      acc[b] = mfma32(alo, bhi, acc[b]);
+    for (int e = 0; e < 8; ++e) {
+      amax = fmaxf(amax, fabsf(x[e]));
+      bmax = fmaxf(bmax, fabsf(y[e]));
     }
+    u32x4 ahi, alo, bhi, blo;
+    split8(x, ahi, alo);
+    split8(y, bhi, blo);
+    acc = mfma32(bhi, ahi, acc);
+    acc = mfma32(blo, ahi, acc);
+    acc = mfma32(bhi, alo, acc);
   }
-  // the two K-halves of every row / column sit in lanes l and l ^ 32
-  a2 += __shfl_xor(a2, 32);
-  for (int off = 16; off > 0; off >>= 1) a2 = fmaxf(a2, __shfl_xor(a2, off));  // max over the 32 rows
-  float tau[2];
-#pragma unroll
-  for (int b = 0; b < 2; ++b) {
-    b2[b] += __shfl_xor(b2[b], 32);
-    tau[b] = 0x1p-13f * fabsf(a.c) * sqrtf(a2 * b2[b]);
-  }
+  // the two K-halves of every row / column sit in lanes l and l ^ 32; then the max over the 32 columns
+  amax = fmaxf(amax, __shfl_xor(amax, 32));
+  for (int off = 32; off > 0; off >>= 1) bmax = fmaxf(bmax, __shfl_xor(bmax, off));
+  // tau: the error bound of the float32 delta, 2^-13 |c| ||A_i|| max_j ||B_:j|| <= 2^-13 |c| r amax bmax;
+  // -1 where delta is exactly zero (a zero A row or all-zero B columns, e.g. B at its zero
+  // initialisation), so that no element is re-decided there
+  const float tau = (amax == 0.f || bmax == 0.f) ? -1.f : 0x1p-13f * fabsf(a.c) * float(a.r) * amax * bmax;
   __syncthreads();  // Phi0 tile staged
 
-  // Rounding decision per element -> LDS as (q & 15) | (in-range ? 0x10 : 0).
+  const int lr = wr + (lane & 31);                            // the lane's row in the tile
+  const bool row_ok = FULL || lr < int(min<int64_t>(a.m - row0, GR_BM));
+  const int kr = int(min<int64_t>(a.k - col0, GR_BN)) - wc - 4 * half;  // the lane's columns 8 g + e < kr are inside
+  auto col_of = [&](int v) { return wc + 8 * (v >> 2) + 4 * half + (v & 3); };
+  auto inside = [&](int v) { return FULL || (row_ok && 8 * (v >> 2) + (v & 3) < kr); };
+
+  // Rounding decision per element from the float32 delta.
+  int ut[16];
+  bool need = false;  // some element of the lane lies within tau of a decision point
 #pragma unroll
-  for (int b = 0; b < 2; ++b) {
-    const int lc = wc + 32 * b + (lane & 31);
-    const int64_t col = col0 + lc;
+  for (int g = 0; g < 4; ++g) {
+    const uint32_t w = read_codes<PACKED>(ph, lr, col_of(4 * g));
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int v = 4 * g + e;
+      float margin;
+      ut[v] = grid_round(code_of<PACKED>(w, e), f, a.c * acc[v], &margin);
+      need |= margin <= tau && inside(v);
+    }
+  }
+  // float64 re-decision of those elements (rare: the wave takes this branch only if one of its lanes needs it)
+  if (__builtin_amdgcn_ballot_w64(need)) {
+    const int64_t row = row0 + lr;
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
-      const int lr = wr + acc_row(v, lane);
-      const int64_t row = row0 + lr;
-      int code;
-      if (a.packed) code = int(uint32_t(ph[lr][lc >> 1]) << (28 - 4 * (lc & 1))) >> 28;
-      else code = int(int8_t(ph[lr][lc]));
+      const int code = code_of<PACKED>(read_codes<PACKED>(ph, lr, col_of(v & 12)), v & 3);
       float margin;
-      int ut = grid_round(code, f, a.c * acc[b][v], &margin);
-      if (margin <= tau[b] && row < a.m && col < a.k) {
-        // float64 re-decision; independent partial sums keep the loads in flight
-        double d0 = 0.0, d1 = 0.0, d2 = 0.0, d3 = 0.0;
+      grid_round(code, f, a.c * acc[v], &margin);
+      if (need && margin <= tau && inside(v)) {
+        const int64_t col = col0 + col_of(v);
+        double d0 = 0.0, d1 = 0.0, d2 = 0.0, d3 = 0.0;  // independent partial sums keep the loads in flight
         int rho = 0;
         for (; rho + 4 <= a.r; rho += 4) {
           d0 = __builtin_fma(double(a.A[row * a.r + rho]), double(a.B[int64_t(rho) * a.k + col]), d0);
@@ -195,49 +204,101 @@ __global__ __launch_bounds__(256) void k_grid(GridArgs a) {
           d3 = __builtin_fma(double(a.A[row * a.r + rho + 3]), double(a.B[int64_t(rho + 3) * a.k + col]), d3);
         }
         for (; rho < a.r; ++rho) d0 = __builtin_fma(double(a.A[row * a.r + rho]), double(a.B[int64_t(rho) * a.k + col]), d0);
-        ut = grid_round_f64(code, f, a.c64 * ((d0 + d1) + (d2 + d3)));
+        ut[v] = grid_round_f64(code, f, a.c64 * ((d0 + d1) + (d2 + d3)));
       }
-      const int q = min(max(ut, lo), hi);
-      qs[lr][lc] = (row < a.m && col < a.k) ? uint8_t((q & 15) | (q == ut ? 0x10 : 0)) : uint8_t(0);
     }
   }
-  __syncthreads();
 
-  // Packed q: row t/4, 32 columns per thread -> 16 bytes.
-  {
-    const int lr = threadIdx.x >> 2, seg = threadIdx.x & 3;
-    const int64_t row = row0 + lr;
-    const int64_t cbase = col0 + 32 * seg;          // first column of this segment
-    if (row < a.m && cbase < a.kq) {
-      uint32_t w[4];
-      #pragma unroll
-      for (int p = 0; p < 4; ++p) {
-        uint32_t acc_w = 0;
-        #pragma unroll
-        for (int e = 0; e < 8; ++e) acc_w |= uint32_t(qs[lr][32 * seg + 8 * p + e] & 15) << (4 * e);
-        w[p] = acc_w;
-      }
-      uint8_t* dst = a.qout + row * a.ldq + (cbase >> 1);
-      if (cbase + 32 <= a.kq && ((reinterpret_cast<uintptr_t>(dst) & 15) == 0)) {
-        *reinterpret_cast<u32x4*>(dst) = u32x4{w[0], w[1], w[2], w[3]};
-      } else {
-        const int64_t nbytes = min<int64_t>(16, (a.kq - cbase + 1) >> 1);
-        for (int64_t byte = 0; byte < nbytes; ++byte) dst[byte] = uint8_t(w[byte >> 2] >> (8 * (byte & 3)));
-      }
-    }
-  }
-  // Clip-mask bits, transposed: bit (row % 8) of byte [col][row / 8]; one
-  // 32-row word per thread (column t % 128, rows 32 (t / 128) .. +31).
-  if (a.mout) {
-    const int c = threadIdx.x & 127, hr = threadIdx.x >> 7;
-    const int64_t col = col0 + c;
-    if (col < a.kq) {
-      uint32_t bitsw = 0;
+  // Clip to the grid; pack the nibbles (cols 8g + 4 half .. +3 -> 16 bits) and
+  // gather the clip-mask bits column by column with wave ballots.
+  // Lane L < 32 writes the mask word of column wc + L: the ballot of element v = 4 (L / 8) + L % 4,
+  // its low half for L % 8 < 4, else its high half.
+  const int myv = 4 * ((lane >> 3) & 3) + (lane & 3);
+  uint64_t mbal = 0;
+  uint32_t P[4];
 #pragma unroll
-      for (int e = 0; e < 32; ++e) bitsw |= uint32_t((qs[32 * hr + e][c] >> 4) & 1) << e;
-      *reinterpret_cast<uint32_t*>(a.mout + col * a.ldm + ((row0 + 32 * hr) >> 3)) = bitsw;
+  for (int g = 0; g < 4; ++g) {
+    uint32_t nib = 0;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int v = 4 * g + e;
+      const bool ok = inside(v);
+      const int q = min(max(ut[v], lo), hi);
+      nib |= uint32_t(ok ? q & 15 : 0) << (4 * e);
+      // lanes 0..31 of the ballot: column 8 g + e of the block; lanes 32..63: that column + 4
+      const uint64_t bal = __builtin_amdgcn_ballot_w64(ok && q == ut[v]);
+      mbal = myv == v ? bal : mbal;
+    }
+    P[g] = nib;
+  }
+  const uint32_t mword = (lane & 4) ? uint32_t(mbal >> 32) : uint32_t(mbal);
+
+  // Packed q: the 8-column word of group g is half 0's nibbles | half 1's << 16;
+  // half 0 stores groups 0-1 and half 1 groups 2-3 (16 columns, 8 bytes each).
+  if (row_ok) {  // lanes l and l ^ 32 share the row, so the exchange partner is active
+    const int64_t row = row0 + lr;
+    const uint32_t send = half ? (P[0] | (P[1] << 16)) : (P[2] | (P[3] << 16));
+    const uint32_t recv = __shfl_xor(send, 32);
+    uint32_t w0, w1;
+    if (half) {
+      w0 = (recv & 0xffffu) | (P[2] << 16);
+      w1 = (recv >> 16) | (P[3] << 16);
+    } else {
+      w0 = P[0] | (recv << 16);
+      w1 = P[1] | (recv & 0xffff0000u);
+    }
+    const int64_t c = col0 + wc + 16 * half;                 // first of the 16 columns
+    uint8_t* dst = a.qout + row * a.ldq + (c >> 1);
+    if (FULL ? (reinterpret_cast<uintptr_t>(dst) & 7) == 0
+             : (c + 16 <= a.kq && (reinterpret_cast<uintptr_t>(dst) & 7) == 0)) {
+      *reinterpret_cast<u32x2*>(dst) = u32x2{w0, w1};
+    } else if (c < a.kq) {
+      const int64_t nb = min<int64_t>(8, (a.kq - c + 1) >> 1);
+      for (int64_t byte = 0; byte < nb; ++byte) dst[byte] = uint8_t((byte < 4 ? w0 : w1) >> (8 * (byte & 3)));
     }
   }
+  // Clip-mask bits, transposed: bit (row % 8) of byte [col][row / 8]; one 32-row word per lane.
+  if (a.mout && lane < 32) {
+    const int64_t col = col0 + wc + lane;
+    if (FULL || col < a.kq) *reinterpret_cast<uint32_t*>(a.mout + col * a.ldm + ((row0 + wr) >> 3)) = mword;
+  }
+}
+
+template <bool PACKED>
+__global__ __launch_bounds__(GR_THREADS) void k_grid(GridArgs a) {
+  __shared__ __attribute__((aligned(16))) uint8_t ph[GR_BM * GR_PITCH];  // the block's Phi0 bytes
+  const int64_t ncb = (a.kq + GR_BN - 1) / GR_BN;
+  const int64_t row0 = int64_t(blockIdx.x / ncb) * GR_BM;
+  const int64_t col0 = int64_t(blockIdx.x % ncb) * GR_BN;
+
+  // Stage the Phi0 tile in LDS first so its loads overlap the rank-r product.
+  // Rows past m read as zeros (buffer range); columns past k are never used.
+  {
+    constexpr int nbytes = (PACKED ? GR_BN / 2 : GR_BN) / 8;  // per thread: 16 (Q8) or 8 (packed)
+    const int64_t cb0 = PACKED ? col0 / 2 : col0;
+    const auto r = grid_rsrc(a.phi0 + row0 * a.ld_phi + cb0, (a.m - row0) * a.ld_phi - cb0);
+    const int tr = threadIdx.x >> 3, seg = threadIdx.x & 7;   // 8 threads per row
+    const int off = int(tr * a.ld_phi) + seg * nbytes;
+    uint8_t* dst = ph + tr * GR_PITCH + seg * nbytes;
+    if ((a.ld_phi & (nbytes - 1)) == 0) {
+      if constexpr (PACKED) {
+        *reinterpret_cast<u32x2*>(dst) = __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0));
+      } else {
+        const u32x4 v = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+        *reinterpret_cast<u32x2*>(dst) = u32x2{v[0], v[1]};
+        *reinterpret_cast<u32x2*>(dst + 8) = u32x2{v[2], v[3]};
+      }
+    } else {
+      for (int o = 0; o < nbytes; ++o) dst[o] = uint8_t(__builtin_amdgcn_raw_buffer_load_b8(r, off + o, 0, 0));
+    }
+  }
+
+  // Interior blocks (every row and column inside the matrix, r a multiple of
+  // 16) take a variant without bounds checks.
+  const bool full = row0 + GR_BM <= a.m && col0 + GR_BN <= a.k && (a.r & 15) == 0 &&
+                    (reinterpret_cast<uintptr_t>(a.A) & 15) == 0;
+  if (full) grid_body<PACKED, true>(a, ph, row0, col0);
+  else grid_body<PACKED, false>(a, ph, row0, col0);
 }
 
 // ============================================================================ activations
@@ -285,7 +346,8 @@ hipError_t launch_encode(const float* W0, const float* s0, int64_t m, int64_t k,
 
 hipError_t launch_grid(const GridArgs& a, hipStream_t st) {
   const int64_t nblocks = ((a.kq + GR_BN - 1) / GR_BN) * ((a.m + GR_BM - 1) / GR_BM);
-  k_grid<<<unsigned(nblocks), 256, 0, st>>>(a);
+  if (a.packed) k_grid<true><<<unsigned(nblocks), GR_THREADS, 0, st>>>(a);
+  else k_grid<false><<<unsigned(nblocks), GR_THREADS, 0, st>>>(a);
   return hipGetLastError();
 }
 
