@@ -10,7 +10,9 @@ differ only when its pre-round value lies within 1e-5 of a .5 boundary, and
 such elements must stay below a 1e-4 fraction); Y, dX, dA, dB within a
 relative Frobenius error of 1e-4 (float32 activations) or 2e-2 (bfloat16).
 """
+import math
 import sys
+from fractions import Fraction
 
 import numpy as np
 import pytest
@@ -257,6 +259,41 @@ def test_stress_rounding_flips_and_clipping(lr):
         _, M, _, _ = O.grid_from_inputs(c.phi0_ref, c.A, c.B, c.L.alpha, c.L.rank, bits, fmt)
         assert (~M).sum() > 200, "stress case should clip"
         check_full(lr, c)
+
+
+def _rne_exact(x):
+    """Round half to even of an exact rational."""
+    fl = math.floor(x)
+    d = x - fl
+    if d != Fraction(1, 2):
+        return fl + (1 if d > Fraction(1, 2) else 0)
+    return fl + (fl & 1)
+
+
+def test_exact_ties_zero_and_tiny_b(lr):
+    """B = 0 (the LoRA initialisation) puts every Q-format code whose fraction is
+    one half on an exact tie, resolved to even; B of order 1e-20 decides the
+    same ties by the sign of a delta far below float64 resolution at 1/2.  Away
+    from the oracle's .5 window the grid must equal the oracle's; inside it, the
+    round-half-to-even of Phi0 + (alpha/r) A B in exact rational arithmetic."""
+    for fmt, bits, b_std in (("q8", 4, 0.0), ("q8", 3, 0.0), ("q8", 4, 1e-20), ("int_packed2", 4, 1e-20)):
+        _log(f"[ties {fmt} b{bits} B std {b_std}]")
+        c = Case(lr, 320, 264, 64, 16, 16.0, bits, fmt, 0, 0, "bf16", seed=21, b_std=b_std)
+        check_setup(c)
+        L = c.L
+        q_dev = O.unpack_int4(lr.lrqat_merge_to_int4(c.spec, c.d_phi0, c.d_A, c.d_B).cpu().numpy())
+        q_ref, _, near, _ = O.grid_from_inputs(c.phi0_ref, c.A, c.B, L.alpha, L.rank, bits, fmt)
+        assert np.array_equal(q_dev[~near], q_ref[~near])
+        phi = O.decode_phi0(c.phi0_ref, bits, fmt)
+        lo, hi = O.grid_limits(bits)
+        cc = Fraction(L.alpha) / L.rank
+        for i, j in np.argwhere(near):
+            d = sum(Fraction(float(c.A[i, t])) * Fraction(float(c.B[t, j])) for t in range(L.rank))
+            want = min(max(_rne_exact(Fraction(float(phi[i, j])) + cc * d), lo), hi)
+            assert q_dev[i, j] == want, (i, j, q_dev[i, j], want)
+        _log(f"  {int(near.sum())} elements on .5 points checked exactly")
+        if b_std == 0.0:
+            check_full(lr, c)
 
 
 def test_accumulate_and_determinism(lr):
