@@ -11,6 +11,9 @@ value = algorithmic flops per step (6 T m k + 8 m k r) / step time, in TFLOP/s.
 roofline: the kernel with the largest share of the step, timed with HIP events
 on the library's stream, against the bf16 dense MFMA peak of 2.5 PFLOP/s.
 cpu_baseline: the CPU oracle on a bounded token sample of the same layer.
+Also reported: per-step p10/p50/p90, the merge (lrqat_merge_to_int4) as
+algorithmic GB/s beside a measured device-copy rate, and the device memory the
+layer holds (analytic, with checkpointing) beside torch's measured peak.
 """
 from __future__ import annotations
 
@@ -175,14 +178,15 @@ def main():
         step()
     torch.cuda.synchronize()
     print(f"[bench] warmup done ({args.warmup} steps)", file=sys.stderr, flush=True)
-    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     torch.cuda.synchronize()
-    ev0.record(stream)
-    for _ in range(args.steps):
+    evs[0].record(stream)
+    for i in range(args.steps):
         step()
-    ev1.record(stream)
+        evs[i + 1].record(stream)
     torch.cuda.synchronize()
-    ms = ev0.elapsed_time(ev1) / args.steps
+    ms = evs[0].elapsed_time(evs[-1]) / args.steps
+    per_step = np.array([evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps)])
     peak_mem = torch.cuda.max_memory_allocated(dev)
     flops = wl.flops_fwd_bwd()
     value = flops / (ms * 1e-3) / 1e12
@@ -207,6 +211,37 @@ def main():
                 "frac": (dom_flops / dom_avg_s / 1e12) / PEAK_BF16_TFLOPS if dom_flops else None,
                 "traffic": traffic}
 
+    # merge (W_Z for inference) and a plain device copy, as bandwidth
+    merge_bytes = phi0.numel() * phi0.element_size() + 4 * (m + k) * r + m * k // 2
+    W_int4 = torch.empty((m, k // 2), dtype=torch.uint8, device=dev)
+    for _ in range(3):
+        lrqat.lrqat_merge_to_int4(spec, phi0, A, B, out=W_int4, stream=stream)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(20):
+        lrqat.lrqat_merge_to_int4(spec, phi0, A, B, out=W_int4, stream=stream)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    merge_us = 1e3 * e0.elapsed_time(e1) / 20
+    src = torch.empty(256 << 18, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    e0.record(stream)
+    for _ in range(10):
+        dst.copy_(src)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    copy_gbs = 2 * src.numel() * 4 * 10 / (e0.elapsed_time(e1) * 1e-3) / 1e9
+    del src, dst
+    merge = {"us": merge_us, "algorithmic_bytes": merge_bytes, "GB/s": merge_bytes / (merge_us * 1e-6) / 1e9,
+             "frac_of_hbm_peak": merge_bytes / (merge_us * 1e-6) / 1e9 / PEAK_HBM_GBS,
+             "device_copy_GB/s": copy_gbs}
+    # device memory the layer holds across forward + backward (checkpointing: nothing saved but the inputs)
+    act_b = 2 if wl.act_dtype == "bf16" else 4
+    analytic = {"phi0": phi0.numel() * phi0.element_size(), "s": s0.numel() * 4, "A+B": 4 * (m + k) * r,
+                "X+dY": act_b * T * (k + m), "Y+dX": act_b * T * (m + k), "dA+dB": 4 * (m + k) * r,
+                "workspace_fwd": ws_f.numel(), "workspace_bwd": ws_b.numel()}
+
     cpu = None
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle sample", file=sys.stderr, flush=True)
@@ -219,9 +254,12 @@ def main():
         "config": {"workload": wl.name, "tokens": T, "out_features": m, "in_features": k, "rank": r,
                    "alpha": wl.alpha, "bits": wl.bits, "phi_format": wl.phi_format, "group_size": wl.group_size,
                    "act_bits": wl.act_bits, "parallelism": "none"},
+        "step_ms_p10_p50_p90": [float(np.percentile(per_step, q)) for q in (10, 50, 90)],
         "pct_of_bf16_peak": 100.0 * value / PEAK_BF16_TFLOPS,
         "tokens_per_s": T / (ms * 1e-3),
         "peak_device_mem_bytes": int(peak_mem),
+        "analytic_mem_bytes": {**analytic, "total": int(sum(analytic.values()))},
+        "merge": merge,
         "kernels": kernels,
         "roofline": roofline,
         "cpu_baseline": cpu,
