@@ -153,7 +153,7 @@ Workspace layout(const Dims& d, int64_t T, bool backward) {
   return w;
 }
 
-GridArgs grid_args(const Dims& d, const void* phi0, const float* A, const float* B, uint8_t* q, uint8_t* mask) {
+GridArgs grid_args(const Dims& d, const void* phi0, const float* A, const float* B, uint8_t* q, uint16_t* mask) {
   GridArgs a{};
   a.phi0 = static_cast<const uint8_t*>(phi0);
   a.ld_phi = d.packed ? d.k / 2 : d.k;
@@ -170,7 +170,7 @@ GridArgs grid_args(const Dims& d, const void* phi0, const float* A, const float*
   a.ldq = d.kpad / 2;
   a.kq = d.kpad;
   a.mout = mask;
-  a.ldm = d.mpad / 8;
+  a.ldm = d.kpad;
   return a;
 }
 
@@ -312,7 +312,7 @@ lrqat_status lrqat_backward(const lrqat_layer* layer, int64_t tokens, const void
     return fail(LRQAT_EWORKSPACE, "workspace of %zu bytes is smaller than the %zu bytes needed", ws_bytes, w.total);
   uint8_t* base = static_cast<uint8_t*>(ws);
   uint8_t* q = base + w.q;
-  uint8_t* mask = base + w.mask;
+  uint16_t* mask = reinterpret_cast<uint16_t*>(base + w.mask);
   const GridArgs ga = grid_args(d, phi0, A, B, q, mask);
   LRQAT_TRY(hip_status(timed("grid", st, [&] { return launch_grid(ga, st); }), "grid"));
 
@@ -322,7 +322,7 @@ lrqat_status lrqat_backward(const lrqat_layer* layer, int64_t tokens, const void
     fa.X = static_cast<const float*>(X);
     fa.dY = static_cast<const float*>(dY);
     fa.q = q; fa.ldq = d.kpad / 2;
-    fa.mask = mask; fa.ldm = d.mpad / 8;
+    fa.mask = mask; fa.ldm = d.kpad;
     fa.s = s; fa.gsize = d.g; fa.ngroups = d.ngroups;
     fa.A = A; fa.B = B;
     fa.G = reinterpret_cast<float*>(base + w.G);
@@ -356,7 +356,7 @@ lrqat_status lrqat_backward(const lrqat_layer* layer, int64_t tokens, const void
   p.ldb = d.act ? d.kpad : d.k;
   p.s = s; p.gsize = d.g; p.ngroups = d.ngroups;
   p.sx = d.act ? sx : nullptr;
-  p.mask = mask; p.ldm = d.mpad / 8;
+  p.mask = mask; p.ldm = d.kpad;
   p.Am = A; p.Bm = B; p.r = int(d.r);
   p.dA_part = dA_part; p.dB_part = dB_part;
   LRQAT_TRY(hip_status(timed("gemm_dw", st, [&] { return launch_gemm(kDw, d.act, d.g != 0, p, st); }), "gemm_dw"));

@@ -76,7 +76,12 @@ __host__ __device__ __forceinline__ int grid_round(int code, int f, float delta,
   const float cw = __builtin_ceilf(w);
   int ut = n + int(cw);
   if (cw == w) ut += ut & 1;
-  if (margin) *margin = __builtin_fabsf(w - __builtin_rintf(w));  // distance to the nearest decision point
+  if (margin) {
+    // distance to the nearest decision point nd, less the rounding error of the
+    // float32 sum there (at most 2^-23 |nd|; the sum is exact near nd = 0)
+    const float nd = __builtin_rintf(w);
+    *margin = __builtin_fabsf(w - nd) - 0x1p-23f * __builtin_fabsf(nd);
+  }
   return ut;
 }
 

@@ -78,12 +78,12 @@ struct StoreOut {
 struct StoreG {  // G = s * M * dW
   float* g;
   int64_t k;
-  const uint8_t* mask;
+  const uint16_t* mask;
   int64_t ldm;
   const float* s;
   int64_t gsize, ngroups;
   __device__ void operator()(int64_t i, int64_t j, float v) const {
-    const int bit = (mask[j * ldm + (i >> 3)] >> (i & 7)) & 1;
+    const int bit = (mask[(i >> 4) * ldm + j] >> (i & 15)) & 1;
     const float sc = gsize ? s[i * ngroups + j / gsize] : s[i];
     g[i * k + j] = bit ? v * sc : 0.f;
   }

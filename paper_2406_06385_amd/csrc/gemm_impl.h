@@ -513,13 +513,18 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     const int64_t rowb = m0 + wm;  // first row of the wave
     uint16_t* Gs = lds;
 
-    // clip-mask bits of the lane's four columns over the wave's 128 rows (transposed layout)
+    // clip-mask bits of the lane's four columns over the wave's 128 rows: word i
+    // holds rows 32 i .. +31 (two 16-row words of the mask)
     u32x4 mbits[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int64_t col = n0 + wn + 32 * j + (lane & 31);
       mbits[j] = u32x4{0u, 0u, 0u, 0u};
-      if (col < p.N) mbits[j] = *reinterpret_cast<const u32x4*>(p.mask + col * p.ldm + (rowb >> 3));
+      if (col < p.N) {
+        const uint16_t* mp = p.mask + (rowb >> 4) * p.ldm + col;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) mbits[j][i] = uint32_t(mp[2 * i * p.ldm]) | (uint32_t(mp[(2 * i + 1) * p.ldm]) << 16);
+      }
     }
     if constexpr (!GRP) {
       const int64_t row = m0 + threadIdx.x;

@@ -58,24 +58,36 @@ __global__ __launch_bounds__(256) void k_encode(const float* __restrict__ W0, co
 }
 
 // ============================================================================ grid
-// Tile 64 rows x 128 columns per block of 8 waves; wave w covers the 32x32
-// block at rows 32*(w/4), columns 32*(w%4).  delta = c A B is an MFMA
-// product of bfloat16 hi/lo splits, A B ~ Ahi Bhi + Ahi Blo + Alo Bhi,
-// accumulated in float32.  Its error is below 3*2^-16 sum_rho |A||B| plus the
-// float32 accumulation, bounded here by 2^-13 |c| ||A_i|| max_j ||B_:j||
-// (Cauchy-Schwarz) <= 2^-13 |c| r max|A_i:| max|B_:j|.  An element whose pre-round value lies within that bound
-// of a rounding decision point is decided again from a float64 delta, so the
-// grid equals the exact one except within float64 rounding of a .5 point.
+// A block owns a strip of 64 columns and 64 * nit rows; in round it
+// (0 .. nit-1) wave w handles the 16-row block 4 it + w.  For a 16 x 64 wave
+// tile, delta = c A B comes from 16x16x32 MFMAs on bfloat16 hi/lo splits,
+// A B ~ Ahi Bhi + Ahi Blo + Alo Bhi, accumulated in float32.  The product is
+// transposed (B columns are the MFMA row operand) and the B columns of column
+// block cb (0..3) are permuted: MFMA row i stands for column
+// 16 (i / 4) + 4 cb + i % 4, so lane l owns weight row l % 16 and the 16
+// consecutive columns 16 (l / 16) .. +15 of the tile.  Its Phi0 codes are one
+// 16-byte (Q8) or 8-byte (packed) load, its q nibbles one 8-byte store, and
+// its clip-mask bits one wave ballot per column.
 //
-// The product is formed transposed (B columns as the MFMA row operand), so a
-// lane owns one weight row and the columns 8 g + 4 (lane / 32) + e
-// (g, e = 0..3) of its wave's block: its Phi0 codes come as one 32-bit (Q8)
-// or 16-bit (packed) LDS read per 4 elements, its q nibbles pack in
-// registers, and the transposed clip mask is one wave ballot per column pair.
-// The pass is latency-bound (one short dependent chain per block), so the
-// per-lane state is kept small for occupancy.
-constexpr int GR_BM = 64, GR_BN = 128, GR_THREADS = 512;
-constexpr int GR_PITCH = 136;  // LDS bytes per staged Phi0 row: 34 dwords keeps the 32 rows of a read on distinct banks
+// Error bound of the float32 delta: the split drops terms below
+// 3.0001 * 2^-16 |a||b| per product; float32 accumulation of the 3r products
+// and the scaling by c add at most (3r + 2) 2^-24 sum |products|.  With
+// Cauchy-Schwarz, sum_rho |A_i,rho||B_rho,j| <= ||A_i:|| ||B_:j||, so
+// |delta32 - delta| <= tau_coef * ||A_i:|| * max_j ||B_:j||, where tau_coef =
+// 1.02 (3 * 2^-16 + (3r + 2) 2^-24) |c| (the 1.02 covers the float32 norms).
+// Near a decision point n != 0 the float32 sum u - n adds at most 2^-23 |n|;
+// near n = 0 it is exact.  Elements inside that bound are decided again from
+// a float64 delta, so the grid equals the exact one except within float64
+// rounding of a .5 point.
+constexpr int GR_COLS = 64, GR_THREADS = 256, GR_MIN_BLOCKS = 2048;
+
+// 16x16x32 MFMA, D(16x16, f32) += P(16x32, bf16) Q(32x16, bf16): lane l
+// supplies row l % 16 of P and column l % 16 of Q, each with the 8 K-values
+// 8 (l / 16) .. +7; D element v of lane l is D[4 (l / 16) + v][l % 16].
+__device__ __forceinline__ f32x4 mfma16(const u32x4& p, const u32x4& q, const f32x4& c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, p), __builtin_bit_cast(bf16x8, q), c, 0, 0,
+                                                 0);
+}
 
 // 8 consecutive floats -> bf16 hi part and bf16 lo part (x - hi), packed.
 __device__ __forceinline__ void split8(const float (&x)[8], u32x4& hi, u32x4& lo) {
@@ -91,214 +103,420 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t grid_rsrc(const void* base, in
   const int64_t n = bytes < 0 ? 0 : (bytes > int64_t(0xFFFFFFFF) ? int64_t(0xFFFFFFFF) : bytes);
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), short(0), int(uint32_t(n)), 0x00020000);
 }
-
-// Phi0 code e (0..3) of a 32-bit word of four Q8 bytes or a 16-bit word of four packed nibbles.
-template <bool PACKED>
-__device__ __forceinline__ int code_of(uint32_t w, int e) {
-  if constexpr (PACKED) return int(w << (28 - 4 * e)) >> 28;
-  else return int(w << (24 - 8 * e)) >> 24;
+__device__ __forceinline__ float gld(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, int(off), 0, 0));
 }
 
-template <bool PACKED>
-__device__ __forceinline__ uint32_t read_codes(const uint8_t* ph, int lr, int lc) {
-  if constexpr (PACKED) return *reinterpret_cast<const uint16_t*>(ph + lr * GR_PITCH + (lc >> 1));
-  else return *reinterpret_cast<const uint32_t*>(ph + lr * GR_PITCH + lc);
+// Upper bound of the Euclidean norm from a float32 sum of squares and the
+// exact max |x| (sqrt(n) max|x| where the squares may have underflowed).
+__device__ __forceinline__ float norm_bound(float ssq, float amax, int n) {
+  return ssq > 0x1p-100f ? __builtin_sqrtf(ssq) : __builtin_sqrtf(float(n)) * amax;
 }
 
-// Decision, packing and mask of one block after its Phi0 tile is staged
-// (the caller's barrier follows the rank-r product inside).
-template <bool PACKED, bool FULL>
-__device__ __forceinline__ void grid_body(const GridArgs& a, const uint8_t* ph, int64_t row0, int64_t col0) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, half = lane >> 5;
-  const int wr = 32 * (wave >> 2), wc = 32 * (wave & 3);
+// The lane's 16 Phi0 codes (columns 16 (l / 16) .. +15 of the tile): four
+// 32-bit words of Q8 bytes, or two words of packed nibbles.
+struct PhiRegs {
+  uint32_t w[4];
+};
+
+// Buffer resources take a wave-uniform base (here the first row of the wave's
+// 16-row block); rows past m read as zeros.
+template <bool PACKED>
+__device__ __forceinline__ void load_phi(PhiRegs& P, const GridArgs& a, int64_t rowblk, int64_t col0, bool vec) {
+  const int lane = threadIdx.x & 63;
+  const int nb = PACKED ? 8 : 16;
+  const int64_t row0 = rowblk * 16, cb0 = PACKED ? col0 / 2 : col0;
+  const auto r = grid_rsrc(a.phi0 + row0 * a.ld_phi + cb0, (a.m - row0) * a.ld_phi - cb0);
+  const uint32_t off = uint32_t((lane & 15) * a.ld_phi + nb * (lane >> 4));
+  if (vec) {
+    if constexpr (PACKED) {
+      const u32x2 v = __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(r, int(off), 0, 0));
+      P.w[0] = v[0];
+      P.w[1] = v[1];
+      P.w[2] = P.w[3] = 0u;
+    } else {
+      const u32x4 v = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, int(off), 0, 0));
+#pragma unroll
+      for (int q = 0; q < 4; ++q) P.w[q] = v[q];
+    }
+  } else {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) P.w[q] = 0u;
+    for (int b = 0; b < nb; ++b)
+      P.w[b >> 2] |= uint32_t(__builtin_amdgcn_raw_buffer_load_b8(r, int(off + b), 0, 0)) << (8 * (b & 3));
+  }
+}
+
+// Code of column 16 (l / 16) + idx (idx = 4 cb + v) of the lane.
+template <bool PACKED>
+__device__ __forceinline__ int phi_code(const PhiRegs& P, int idx) {
+  if constexpr (PACKED) return int(P.w[idx >> 3] << (28 - 4 * (idx & 7))) >> 28;
+  else return int(P.w[idx >> 2] << (24 - 8 * (idx & 3))) >> 24;
+}
+
+// The same with a run-time index (the rare float64 path).
+template <bool PACKED>
+__device__ __forceinline__ int phi_code_dyn(const PhiRegs& P, int idx) {
+  const int wi = PACKED ? idx >> 3 : idx >> 2;
+  const uint32_t w = wi == 0 ? P.w[0] : wi == 1 ? P.w[1] : wi == 2 ? P.w[2] : P.w[3];
+  if constexpr (PACKED) return int(w << (28 - 4 * (idx & 7))) >> 28;
+  else return int(w << (24 - 8 * (idx & 3))) >> 24;
+}
+
+// A operand of one K-step: A[row][32 ks + 8 (l / 16) .. +7] of the lane's
+// row (zero past r or m).
+__device__ __forceinline__ void load_a(float (&x)[8], const GridArgs& a, int64_t rowblk, int ks, bool avec) {
+  const int lane = threadIdx.x & 63;
+  const int rb = 32 * ks + 8 * (lane >> 4);
+  const int64_t row0 = rowblk * 16;
+  const auto r = grid_rsrc(a.A + row0 * a.r, (a.m - row0) * int64_t(a.r) * 4);
+  const uint32_t off = uint32_t(((lane & 15) * a.r + rb) * 4);
+  if (avec) {
+    const f32x4 u = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, int(off), 0, 0));
+    const f32x4 w = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, int(off + 16), 0, 0));
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      x[e] = u[e];
+      x[4 + e] = w[e];
+    }
+  } else {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {  // unconditional loads, then ranks >= r are zeroed
+      const float v = gld(r, off + 4 * e);
+      x[e] = rb + e < a.r ? v : 0.f;
+    }
+  }
+}
+
+// B operand of one K-step and column block cb: B[32 ks + 8 (l / 16) + e][col of MFMA row l % 16]
+// (zero past r or k).
+__device__ __forceinline__ void load_b(float (&y)[8], const GridArgs& a, int64_t col0, int cb, int ks) {
+  const int lane = threadIdx.x & 63, i = lane & 15;
+  const int64_t lc = 16 * (i >> 2) + 4 * cb + (i & 3);
+  const int rb = 32 * ks + 8 * (lane >> 4);
+  const auto r = grid_rsrc(a.B + col0, int64_t(a.r) * a.k * 4 - col0 * 4);
+  // unconditional loads (ranks >= r lie past the buffer's range and read as
+  // zeros), then columns >= k are zeroed: no branch around a load
+  const bool col_ok = col0 + lc < a.k;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const float v = gld(r, uint32_t(((rb + e) * a.k + lc) * 4));
+    y[e] = col_ok ? v : 0.f;
+  }
+}
+
+// Rounding decision, clip, packing and mask of one 16 x 64 wave tile.
+//
+// Fast path: with Phi0 = n + cf 2^-f (n = floor, cf the f fraction bits),
+// u = n + 1/2 + w and w = (cf 2^-f - 1/2) + delta, evaluated as one fused
+// multiply-add from exact terms.  For w in (-1, 1) and w != 0 the nearest
+// integer to u is n + [w > 0].  The answer is certain unless |w| lies within
+// the error bound tau of 0, or |w| is at least 1 - tau (a decision point at
+// +-1, or beyond); a wave with such an element redoes its tile with exact
+// margins and float64 deltas (rare).  Where delta is identically zero on the
+// strip (B = 0, the adapters' initial state) the grid is round-half-even of
+// Phi0, decided in integers.
+template <bool PACKED, bool MASK>
+__device__ __forceinline__ void grid_finish(const GridArgs& a, const PhiRegs& P, const f32x4 (&acc)[4], float tau,
+                                            bool zero_delta, int64_t row, int64_t c16, int64_t rowblk, int64_t col0) {
+  const int lane = threadIdx.x & 63;
   const int lo = -(1 << (a.bits - 1)), hi = (1 << (a.bits - 1)) - 1;
   const int f = PACKED ? 0 : 8 - a.bits;
+  const bool row_ok = row < a.m;
+  const int kin = int(max<int64_t>(0, min<int64_t>(16, a.k - c16)));  // the lane's columns inside k
+  auto n_of = [&](int idx) { return PACKED ? phi_code<true>(P, idx) : phi_code<false>(P, idx) >> f; };
 
-  // acc[v] = (A B)[row0 + wr + lane % 32][col0 + wc + acc_row(v, lane)]
-  f32x16 acc;
-#pragma unroll
-  for (int v = 0; v < 16; ++v) acc[v] = 0.f;
-
-  const int64_t arow = row0 + wr + (lane & 31);
-  const int64_t bcol = col0 + wc + (lane & 31);
-  const bool avec = FULL || ((a.r & 3) == 0 && (reinterpret_cast<uintptr_t>(a.A) & 15) == 0);
-  // max |A| over the lane's row and max |B| over its column: ||x|| <= sqrt(r) max|x| bounds the
-  // norms, and a zero maximum means an exactly zero delta
-  float amax = 0.f, bmax = 0.f;
-  for (int r0 = 0; r0 < a.r; r0 += 16) {
-    // A operand: A[arow][r0 + 8*half + e]; B operand: B[r0 + 8*half + e][bcol]
-    float x[8], y[8];
-    const int rb = r0 + 8 * half;
-    if (FULL || (avec && arow < a.m && rb + 8 <= a.r)) {
-      const f32x4 u = *reinterpret_cast<const f32x4*>(a.A + arow * a.r + rb);
-      const f32x4 w = *reinterpret_cast<const f32x4*>(a.A + arow * a.r + rb + 4);
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        x[e] = u[e];
-        x[4 + e] = w[e];
-      }
-    } else {
-#pragma unroll
-      for (int e = 0; e < 8; ++e) x[e] = (arow < a.m && rb + e < a.r) ? a.A[arow * a.r + rb + e] : 0.f;
-    }
-#pragma unroll
-    for (int e = 0; e < 8; ++e)
-      y[e] = (FULL || (bcol < a.k && rb + e < a.r)) ? a.B[int64_t(rb + e) * a.k + bcol] : 0.f;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      amax = fmaxf(amax, fabsf(x[e]));
-      bmax = fmaxf(bmax, fabsf(y[e]));
-    }
-    u32x4 ahi, alo, bhi, blo;
-    split8(x, ahi, alo);
-    split8(y, bhi, blo);
-    acc = mfma32(bhi, ahi, acc);
-    acc = mfma32(blo, ahi, acc);
-    acc = mfma32(bhi, alo, acc);
-  }
-  // the two K-halves of every row / column sit in lanes l and l ^ 32; then the max over the 32 columns
-  amax = fmaxf(amax, __shfl_xor(amax, 32));
-  for (int off = 32; off > 0; off >>= 1) bmax = fmaxf(bmax, __shfl_xor(bmax, off));
-  // tau: the error bound of the float32 delta, 2^-13 |c| ||A_i|| max_j ||B_:j|| <= 2^-13 |c| r amax bmax;
-  // -1 where delta is exactly zero (a zero A row or all-zero B columns, e.g. B at its zero
-  // initialisation), so that no element is re-decided there
-  const float tau = (amax == 0.f || bmax == 0.f) ? -1.f : 0x1p-13f * fabsf(a.c) * float(a.r) * amax * bmax;
-  __syncthreads();  // Phi0 tile staged
-
-  const int lr = wr + (lane & 31);                            // the lane's row in the tile
-  const bool row_ok = FULL || lr < int(min<int64_t>(a.m - row0, GR_BM));
-  const int kr = int(min<int64_t>(a.k - col0, GR_BN)) - wc - 4 * half;  // the lane's columns 8 g + e < kr are inside
-  auto col_of = [&](int v) { return wc + 8 * (v >> 2) + 4 * half + (v & 3); };
-  auto inside = [&](int v) { return FULL || (row_ok && 8 * (v >> 2) + (v & 3) < kr); };
-
-  // Rounding decision per element from the float32 delta.
   int ut[16];
-  bool need = false;  // some element of the lane lies within tau of a decision point
+  if (zero_delta) {
+    // round-half-even of Phi0 = n + cf 2^-f
+    const int half = f ? 1 << (f - 1) : 0;
 #pragma unroll
-  for (int g = 0; g < 4; ++g) {
-    const uint32_t w = read_codes<PACKED>(ph, lr, col_of(4 * g));
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int v = 4 * g + e;
-      float margin;
-      ut[v] = grid_round(code_of<PACKED>(w, e), f, a.c * acc[v], &margin);
-      need |= margin <= tau && inside(v);
+    for (int idx = 0; idx < 16; ++idx) {
+      const int code = phi_code<PACKED>(P, idx), n = code >> f, cf = code & ((1 << f) - 1);
+      ut[idx] = f ? n + int(cf > half || (cf == half && (n & 1))) : code;
     }
-  }
-  // float64 re-decision of those elements (rare: the wave takes this branch only if one of its lanes needs it)
-  if (__builtin_amdgcn_ballot_w64(need)) {
-    const int64_t row = row0 + lr;
+  } else {
+    const float tz = fmaxf(tau, 0.f), thr = 1.f - tz - 0x1p-22f;
+    const float sf = __builtin_bit_cast(float, uint32_t(127 - f) << 23);  // 2^-f
+    uint64_t flag = 0;
+    // fraction bits of the four codes of each word, as unsigned bytes (Q8 only)
+    uint32_t fw[4];
 #pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      const int code = code_of<PACKED>(read_codes<PACKED>(ph, lr, col_of(v & 12)), v & 3);
-      float margin;
-      grid_round(code, f, a.c * acc[v], &margin);
-      if (need && margin <= tau && inside(v)) {
-        const int64_t col = col0 + col_of(v);
-        double d0 = 0.0, d1 = 0.0, d2 = 0.0, d3 = 0.0;  // independent partial sums keep the loads in flight
-        int rho = 0;
-        for (; rho + 4 <= a.r; rho += 4) {
-          d0 = __builtin_fma(double(a.A[row * a.r + rho]), double(a.B[int64_t(rho) * a.k + col]), d0);
-          d1 = __builtin_fma(double(a.A[row * a.r + rho + 1]), double(a.B[int64_t(rho + 1) * a.k + col]), d1);
-          d2 = __builtin_fma(double(a.A[row * a.r + rho + 2]), double(a.B[int64_t(rho + 2) * a.k + col]), d2);
-          d3 = __builtin_fma(double(a.A[row * a.r + rho + 3]), double(a.B[int64_t(rho + 3) * a.k + col]), d3);
+    for (int q = 0; q < 4; ++q) fw[q] = P.w[q] & (0x01010101u * uint32_t((1 << f) - 1));
+#pragma unroll
+    for (int idx = 0; idx < 16; ++idx) {
+      const float x = PACKED ? -0.5f : __builtin_fmaf(float((fw[idx >> 2] >> (8 * (idx & 3))) & 0xffu), sf, -0.5f);
+      const float w = __builtin_fmaf(acc[idx >> 2][idx & 3], a.c, x);
+      flag |= __builtin_amdgcn_ballot_w64(fabsf(w) <= tz);
+      flag |= __builtin_amdgcn_ballot_w64(fabsf(w) >= thr);
+      ut[idx] = n_of(idx) + int(w > 0.f);
+    }
+    if (flag) {
+      // exact margins and float64 re-decision for the lanes' elements within the bound
+      uint32_t need = 0;
+#pragma unroll
+      for (int idx = 0; idx < 16; ++idx) {
+        float margin;
+        ut[idx] = grid_round(phi_code<PACKED>(P, idx), f, a.c * acc[idx >> 2][idx & 3], &margin);
+        need |= uint32_t(margin <= tau && row_ok && idx < kin) << idx;
+      }
+      while (__builtin_amdgcn_ballot_w64(need != 0)) {
+        const bool mine = need != 0;
+        const int idx = mine ? __builtin_ctz(need) : -1;
+        need &= need - 1;
+        int unew = 0;
+        if (mine) {
+          const int64_t col = c16 + idx;
+          const float* Ar = a.A + row * a.r;
+          const float* Bc = a.B + col;
+          double d0 = 0.0, d1 = 0.0, d2 = 0.0, d3 = 0.0;  // independent partial sums keep the loads in flight
+          int rho = 0;
+#pragma unroll 1
+          for (; rho + 4 <= a.r; rho += 4) {
+            d0 = __builtin_fma(double(Ar[rho]), double(Bc[int64_t(rho) * a.k]), d0);
+            d1 = __builtin_fma(double(Ar[rho + 1]), double(Bc[int64_t(rho + 1) * a.k]), d1);
+            d2 = __builtin_fma(double(Ar[rho + 2]), double(Bc[int64_t(rho + 2) * a.k]), d2);
+            d3 = __builtin_fma(double(Ar[rho + 3]), double(Bc[int64_t(rho + 3) * a.k]), d3);
+          }
+#pragma unroll 1
+          for (; rho < a.r; ++rho) d0 = __builtin_fma(double(Ar[rho]), double(Bc[int64_t(rho) * a.k]), d0);
+          unew = grid_round_f64(phi_code_dyn<PACKED>(P, idx), f, a.c64 * ((d0 + d1) + (d2 + d3)));
         }
-        for (; rho < a.r; ++rho) d0 = __builtin_fma(double(a.A[row * a.r + rho]), double(a.B[int64_t(rho) * a.k + col]), d0);
-        ut[v] = grid_round_f64(code, f, a.c64 * ((d0 + d1) + (d2 + d3)));
+#pragma unroll
+        for (int j = 0; j < 16; ++j) ut[j] = j == idx ? unew : ut[j];
       }
     }
   }
 
-  // Clip to the grid; pack the nibbles (cols 8g + 4 half .. +3 -> 16 bits) and
-  // gather the clip-mask bits column by column with wave ballots.
-  // Lane L < 32 writes the mask word of column wc + L: the ballot of element v = 4 (L / 8) + L % 4,
-  // its low half for L % 8 < 4, else its high half.
-  const int myv = 4 * ((lane >> 3) & 3) + (lane & 3);
+  // Clip and pack 16 nibbles (8 bytes; columns >= k are written as 0).  Mask:
+  // lane L writes the 16-row word of tile column L = 16 (L / 16) + idx,
+  // idx = L % 16, which is bits 16 (L / 16) .. +15 of the ballot of element idx.
+  uint32_t w0 = 0, w1 = 0;
   uint64_t mbal = 0;
-  uint32_t P[4];
 #pragma unroll
-  for (int g = 0; g < 4; ++g) {
-    uint32_t nib = 0;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int v = 4 * g + e;
-      const bool ok = inside(v);
-      const int q = min(max(ut[v], lo), hi);
-      nib |= uint32_t(ok ? q & 15 : 0) << (4 * e);
-      // lanes 0..31 of the ballot: column 8 g + e of the block; lanes 32..63: that column + 4
-      const uint64_t bal = __builtin_amdgcn_ballot_w64(ok && q == ut[v]);
-      mbal = myv == v ? bal : mbal;
+  for (int idx = 0; idx < 16; ++idx) {
+    const int q = min(max(ut[idx], lo), hi);
+    const uint32_t nib = uint32_t(q & 15) << (4 * (idx & 7));
+    if (idx < 8) w0 |= nib;
+    else w1 |= nib;
+    if constexpr (MASK) {
+      const uint64_t bal = __builtin_amdgcn_ballot_w64(q == ut[idx]);
+      mbal = (lane & 15) == idx ? bal : mbal;
     }
-    P[g] = nib;
   }
-  const uint32_t mword = (lane & 4) ? uint32_t(mbal >> 32) : uint32_t(mbal);
-
-  // Packed q: the 8-column word of group g is half 0's nibbles | half 1's << 16;
-  // half 0 stores groups 0-1 and half 1 groups 2-3 (16 columns, 8 bytes each).
-  if (row_ok) {  // lanes l and l ^ 32 share the row, so the exchange partner is active
-    const int64_t row = row0 + lr;
-    const uint32_t send = half ? (P[0] | (P[1] << 16)) : (P[2] | (P[3] << 16));
-    const uint32_t recv = __shfl_xor(send, 32);
-    uint32_t w0, w1;
-    if (half) {
-      w0 = (recv & 0xffffu) | (P[2] << 16);
-      w1 = (recv >> 16) | (P[3] << 16);
-    } else {
-      w0 = P[0] | (recv << 16);
-      w1 = P[1] | (recv & 0xffff0000u);
-    }
-    const int64_t c = col0 + wc + 16 * half;                 // first of the 16 columns
-    uint8_t* dst = a.qout + row * a.ldq + (c >> 1);
-    if (FULL ? (reinterpret_cast<uintptr_t>(dst) & 7) == 0
-             : (c + 16 <= a.kq && (reinterpret_cast<uintptr_t>(dst) & 7) == 0)) {
+  if (kin < 16) {
+    const uint64_t keep = (uint64_t(1) << (4 * kin)) - 1;  // kin <= 15
+    w0 &= uint32_t(keep);
+    w1 &= uint32_t(keep >> 32);
+  }
+  if (row_ok && c16 < a.kq) {
+    uint8_t* dst = a.qout + row * a.ldq + (c16 >> 1);
+    if (c16 + 16 <= a.kq && (reinterpret_cast<uintptr_t>(dst) & 7) == 0) {
       *reinterpret_cast<u32x2*>(dst) = u32x2{w0, w1};
-    } else if (c < a.kq) {
-      const int64_t nb = min<int64_t>(8, (a.kq - c + 1) >> 1);
-      for (int64_t byte = 0; byte < nb; ++byte) dst[byte] = uint8_t((byte < 4 ? w0 : w1) >> (8 * (byte & 3)));
+    } else {
+      const int64_t nbytes = min<int64_t>(8, (a.kq - c16 + 1) >> 1);
+      for (int64_t b = 0; b < nbytes; ++b) dst[b] = uint8_t((b < 4 ? w0 : w1) >> (8 * (b & 3)));
     }
   }
-  // Clip-mask bits, transposed: bit (row % 8) of byte [col][row / 8]; one 32-row word per lane.
-  if (a.mout && lane < 32) {
-    const int64_t col = col0 + wc + lane;
-    if (FULL || col < a.kq) *reinterpret_cast<uint32_t*>(a.mout + col * a.ldm + ((row0 + wr) >> 3)) = mword;
+  if constexpr (MASK) {
+    const int64_t col = col0 + lane;
+    if (col < a.kq) a.mout[rowblk * a.ldm + col] = uint16_t(mbal >> (16 * (lane >> 4)));
   }
 }
 
-template <bool PACKED>
+// COAL (r = 32, 16-byte aligned A and B rows, k % 4 == 0): B and A are read
+// with coalesced 16-byte loads and rearranged into MFMA operand order in the
+// wave's LDS region; otherwise each lane loads its own operand values.
+template <bool PACKED, bool ONEK, bool MASK, bool COAL>
 __global__ __launch_bounds__(GR_THREADS) void k_grid(GridArgs a) {
-  __shared__ __attribute__((aligned(16))) uint8_t ph[GR_BM * GR_PITCH];  // the block's Phi0 bytes
-  const int64_t ncb = (a.kq + GR_BN - 1) / GR_BN;
-  const int64_t row0 = int64_t(blockIdx.x / ncb) * GR_BM;
-  const int64_t col0 = int64_t(blockIdx.x % ncb) * GR_BN;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x >> 6));
+  // the block's 4 waves cover 256 adjacent columns (whole 128-byte lines of q
+  // and of Q8 Phi0) of the same nit 16-row blocks
+  const int64_t nstrips = (a.kq + 4 * GR_COLS - 1) / (4 * GR_COLS);
+  const int64_t col0 = int64_t(blockIdx.x % nstrips) * 4 * GR_COLS + GR_COLS * wave;
+  const int64_t rb0 = int64_t(blockIdx.x / nstrips) * a.nit;  // first 16-row block of the block
+  const int64_t c16 = col0 + 16 * (lane >> 4);                // the lane's first column
+  const int nks = (a.r + 31) / 32;
+  const bool avec = (a.r & 31) == 0 && (reinterpret_cast<uintptr_t>(a.A) & 15) == 0;
+  // 16-byte (8-byte) code loads need aligned rows; loads past the end of a row
+  // only feed columns >= k, which are never used
+  const bool pvec = ((a.ld_phi | int64_t(reinterpret_cast<uintptr_t>(a.phi0))) & (PACKED ? 7 : 15)) == 0;
 
-  // Stage the Phi0 tile in LDS first so its loads overlap the rank-r product.
-  // Rows past m read as zeros (buffer range); columns past k are never used.
-  {
-    constexpr int nbytes = (PACKED ? GR_BN / 2 : GR_BN) / 8;  // per thread: 16 (Q8) or 8 (packed)
-    const int64_t cb0 = PACKED ? col0 / 2 : col0;
-    const auto r = grid_rsrc(a.phi0 + row0 * a.ld_phi + cb0, (a.m - row0) * a.ld_phi - cb0);
-    const int tr = threadIdx.x >> 3, seg = threadIdx.x & 7;   // 8 threads per row
-    const int off = int(tr * a.ld_phi) + seg * nbytes;
-    uint8_t* dst = ph + tr * GR_PITCH + seg * nbytes;
-    if ((a.ld_phi & (nbytes - 1)) == 0) {
-      if constexpr (PACKED) {
-        *reinterpret_cast<u32x2*>(dst) = __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0));
-      } else {
-        const u32x4 v = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
-        *reinterpret_cast<u32x2*>(dst) = u32x2{v[0], v[1]};
-        *reinterpret_cast<u32x2*>(dst + 8) = u32x2{v[2], v[3]};
+  // The wave's B columns: for r <= 32 (one K-step) their bf16 hi/lo fragments
+  // stay in the wave's own LDS region for all its rounds, else they are
+  // reloaded per K-step.  The largest column norm and |B| of the wave's 64
+  // columns bound the error.
+  __shared__ __attribute__((aligned(16))) u32x4 bfrag[4][2][4][64];
+  __shared__ __attribute__((aligned(16))) float arow[COAL ? 4 : 1][16][36];  // COAL: the tile's A rows (144-byte pitch)
+  float bss = 0.f, bmx = 0.f;
+  if constexpr (COAL) {
+    // B[0..31][col0 .. col0 + 63]: 8 loads of 4 rank rows x 256 bytes, staged raw
+    // in the wave's fragment region, then read back in operand order
+    float* raw = reinterpret_cast<float*>(&bfrag[wave][0][0][0]);
+    const auto rb = grid_rsrc(a.B + col0, int64_t(a.r) * a.k * 4 - col0 * 4);
+    const int cl = 4 * (lane & 15);
+    u32x4 v[8];
+#pragma unroll
+    for (int t = 0; t < 8; ++t)
+      v[t] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                                           rb, int(uint32_t(((4 * t + (lane >> 4)) * a.k + cl) * 4)), 0, 0));
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) v[t][j] = col0 + cl + j < a.k ? v[t][j] : 0u;
+      *reinterpret_cast<u32x4*>(raw + (4 * t + (lane >> 4)) * 64 + cl) = v[t];
+    }
+    float y[4][8];
+    float ss[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int cb = 0; cb < 4; ++cb)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        y[cb][e] = raw[(8 * (lane >> 4) + e) * 64 + 16 * ((lane & 15) >> 2) + 4 * cb + (lane & 3)];
+        ss[cb] = __builtin_fmaf(y[cb][e], y[cb][e], ss[cb]);
+        bmx = fmaxf(bmx, fabsf(y[cb][e]));
       }
-    } else {
-      for (int o = 0; o < nbytes; ++o) dst[o] = uint8_t(__builtin_amdgcn_raw_buffer_load_b8(r, off + o, 0, 0));
+#pragma unroll
+    for (int cb = 0; cb < 4; ++cb) {
+      u32x4 h, l;
+      split8(y[cb], h, l);
+      bfrag[wave][0][cb][lane] = h;
+      bfrag[wave][1][cb][lane] = l;
+      ss[cb] += __shfl_xor(ss[cb], 16);
+      ss[cb] += __shfl_xor(ss[cb], 32);
+      bss = fmaxf(bss, ss[cb]);
+    }
+    for (int off = 1; off < 64; off <<= 1) {
+      bss = fmaxf(bss, __shfl_xor(bss, off));
+      bmx = fmaxf(bmx, __shfl_xor(bmx, off));
+    }
+  } else {
+    float ss[4] = {0.f, 0.f, 0.f, 0.f};
+    for (int ks = 0; ks < nks; ++ks) {
+#pragma unroll
+      for (int cb = 0; cb < 4; ++cb) {
+        float y[8];
+        load_b(y, a, col0, cb, ks);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          ss[cb] = __builtin_fmaf(y[e], y[e], ss[cb]);
+          bmx = fmaxf(bmx, fabsf(y[e]));
+        }
+        if (ONEK) {
+          u32x4 h, l;
+          split8(y, h, l);
+          bfrag[wave][0][cb][lane] = h;
+          bfrag[wave][1][cb][lane] = l;
+        }
+      }
+    }
+    // the 4 lanes l % 16 + 16 g hold the 4 rank slices of a column
+#pragma unroll
+    for (int cb = 0; cb < 4; ++cb) {
+      ss[cb] += __shfl_xor(ss[cb], 16);
+      ss[cb] += __shfl_xor(ss[cb], 32);
+      bss = fmaxf(bss, ss[cb]);
+    }
+    for (int off = 1; off < 64; off <<= 1) {
+      bss = fmaxf(bss, __shfl_xor(bss, off));
+      bmx = fmaxf(bmx, __shfl_xor(bmx, off));
     }
   }
+  const float nb = norm_bound(bss, bmx, a.r);
 
-  // Interior blocks (every row and column inside the matrix, r a multiple of
-  // 16) take a variant without bounds checks.
-  const bool full = row0 + GR_BM <= a.m && col0 + GR_BN <= a.k && (a.r & 15) == 0 &&
-                    (reinterpret_cast<uintptr_t>(a.A) & 15) == 0;
-  if (full) grid_body<PACKED, true>(a, ph, row0, col0);
-  else grid_body<PACKED, false>(a, ph, row0, col0);
+  int64_t rowblk = rb0;
+  PhiRegs P;
+  float xa[8];
+  u32x4 xc[2];  // COAL: the 16 A rows of a tile, rows lane / 8 and 8 + lane / 8, 16-byte chunk lane % 8
+  auto load_a_coal = [&](int64_t rblk) {
+    const auto r = grid_rsrc(a.A + rblk * 16 * 32, (a.m - rblk * 16) * 128);
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+      xc[h] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, 1024 * h + 16 * lane, 0, 0));
+  };
+  load_phi<PACKED>(P, a, rowblk, col0, pvec);
+  if constexpr (COAL) load_a_coal(rowblk);
+  else if (ONEK) load_a(xa, a, rowblk, 0, avec);
+  for (int it = 0; it < a.nit; ++it, ++rowblk) {
+    if (rowblk * 16 >= a.m) break;  // wave-uniform
+    const int64_t row = rowblk * 16 + (lane & 15);
+    f32x4 acc[4];
+#pragma unroll
+    for (int cb = 0; cb < 4; ++cb) acc[cb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    float ass = 0.f, amx = 0.f;
+    const PhiRegs Pc = P;
+    if (ONEK) {
+      float x[8];
+      if constexpr (COAL) {
+        // through the wave's LDS rows: lane l takes row l % 16, ranks 8 (l / 16) .. +7
+#pragma unroll
+        for (int h = 0; h < 2; ++h) *reinterpret_cast<u32x4*>(&arow[wave][8 * h + (lane >> 3)][4 * (lane & 7)]) = xc[h];
+        const f32x4 u = *reinterpret_cast<const f32x4*>(&arow[wave][lane & 15][8 * (lane >> 4)]);
+        const f32x4 w = *reinterpret_cast<const f32x4*>(&arow[wave][lane & 15][8 * (lane >> 4) + 4]);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          x[e] = u[e];
+          x[4 + e] = w[e];
+        }
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) x[e] = xa[e];
+      }
+      // prefetch the next round's Phi0 codes and A slice
+      if (it + 1 < a.nit) {
+        load_phi<PACKED>(P, a, rowblk + 1, col0, pvec);
+        if constexpr (COAL) load_a_coal(rowblk + 1);
+        else load_a(xa, a, rowblk + 1, 0, avec);
+      }
+      u32x4 ah, al;
+      split8(x, ah, al);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        ass = __builtin_fmaf(x[e], x[e], ass);
+        amx = fmaxf(amx, fabsf(x[e]));
+      }
+#pragma unroll
+      for (int cb = 0; cb < 4; ++cb) {
+        const u32x4 ph = bfrag[wave][0][cb][lane], pl = bfrag[wave][1][cb][lane];
+        acc[cb] = mfma16(ph, ah, acc[cb]);
+        acc[cb] = mfma16(pl, ah, acc[cb]);
+        acc[cb] = mfma16(ph, al, acc[cb]);
+      }
+    } else {
+      if (it + 1 < a.nit) load_phi<PACKED>(P, a, rowblk + 1, col0, pvec);
+      for (int ks = 0; ks < nks; ++ks) {
+        float x[8];
+        load_a(x, a, rowblk, ks, avec);
+        u32x4 ah, al;
+        split8(x, ah, al);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          ass = __builtin_fmaf(x[e], x[e], ass);
+          amx = fmaxf(amx, fabsf(x[e]));
+        }
+#pragma unroll
+        for (int cb = 0; cb < 4; ++cb) {
+          float y[8];
+          load_b(y, a, col0, cb, ks);
+          u32x4 ph, pl;
+          split8(y, ph, pl);
+          acc[cb] = mfma16(ph, ah, acc[cb]);
+          acc[cb] = mfma16(pl, ah, acc[cb]);
+          acc[cb] = mfma16(ph, al, acc[cb]);
+        }
+      }
+    }
+    // row norm: the 4 lanes l % 16 + 16 g hold the 4 rank slices of the row
+    ass += __shfl_xor(ass, 16);
+    ass += __shfl_xor(ass, 32);
+    amx = fmaxf(amx, __shfl_xor(amx, 16));
+    amx = fmaxf(amx, __shfl_xor(amx, 32));
+    // -1 where delta is exactly zero (a zero A row or zero B columns, e.g. B at its zero
+    // initialisation), so that no element is re-decided there
+    const float tau = amx == 0.f ? -1.f : a.tau_coef * norm_bound(ass, amx, a.r) * nb;
+    grid_finish<PACKED, MASK>(a, Pc, acc, tau, bmx == 0.f, row, c16, rowblk, col0);
+  }
 }
 
 // ============================================================================ activations
@@ -344,10 +562,36 @@ hipError_t launch_encode(const float* W0, const float* s0, int64_t m, int64_t k,
   return hipGetLastError();
 }
 
-hipError_t launch_grid(const GridArgs& a, hipStream_t st) {
-  const int64_t nblocks = ((a.kq + GR_BN - 1) / GR_BN) * ((a.m + GR_BM - 1) / GR_BM);
-  if (a.packed) k_grid<true><<<unsigned(nblocks), GR_THREADS, 0, st>>>(a);
-  else k_grid<false><<<unsigned(nblocks), GR_THREADS, 0, st>>>(a);
+hipError_t launch_grid(const GridArgs& a0, hipStream_t st) {
+  GridArgs a = a0;
+  const int64_t nstrips = (a.kq + 4 * GR_COLS - 1) / (4 * GR_COLS), nrb = (a.m + 15) / 16;
+  // 16-row rounds per wave: the most (up to 8) that still gives GR_MIN_BLOCKS blocks
+  a.nit = 8;
+  while (a.nit > 1 && nstrips * ((nrb + a.nit - 1) / a.nit) < GR_MIN_BLOCKS) a.nit /= 2;
+  const int64_t nblocks = nstrips * ((nrb + a.nit - 1) / a.nit);
+  a.tau_coef = float(1.02 * (3.0 * 0x1p-16 + (3.0 * a.r + 2.0) * 0x1p-24) * (a.c < 0 ? -a.c : a.c));
+  const unsigned nb = unsigned(nblocks);
+  const bool coal = a.r == 32 && a.k % 4 == 0 && (reinterpret_cast<uintptr_t>(a.A) & 15) == 0 &&
+                    (reinterpret_cast<uintptr_t>(a.B) & 15) == 0;
+  const int sel = (a.packed ? 8 : 0) | (a.r <= 32 ? 4 : 0) | (coal ? 2 : 0) | (a.mout ? 1 : 0);
+  switch (sel) {
+#define LRQAT_GRID_CASE(S, P, O, C, M) \
+  case S: k_grid<P, O, M, C><<<nb, GR_THREADS, 0, st>>>(a); break;
+    LRQAT_GRID_CASE(0, false, false, false, false)
+    LRQAT_GRID_CASE(1, false, false, false, true)
+    LRQAT_GRID_CASE(4, false, true, false, false)
+    LRQAT_GRID_CASE(5, false, true, false, true)
+    LRQAT_GRID_CASE(6, false, true, true, false)
+    LRQAT_GRID_CASE(7, false, true, true, true)
+    LRQAT_GRID_CASE(8, true, false, false, false)
+    LRQAT_GRID_CASE(9, true, false, false, true)
+    LRQAT_GRID_CASE(12, true, true, false, false)
+    LRQAT_GRID_CASE(13, true, true, false, true)
+    LRQAT_GRID_CASE(14, true, true, true, false)
+    LRQAT_GRID_CASE(15, true, true, true, true)
+#undef LRQAT_GRID_CASE
+    default: return hipErrorInvalidValue;
+  }
   return hipGetLastError();
 }
 

@@ -20,8 +20,10 @@ struct GridArgs {
   uint8_t* qout;         // packed q [m][ldq]
   int64_t ldq;           // bytes per row of qout
   int64_t kq;            // columns written per row of qout (>= k; columns >= k are 0)
-  uint8_t* mout;         // clip-mask bits, transposed: bit (row % 8) of byte [col][row / 8] (nullable)
-  int64_t ldm;           // bytes per column of mout (rows padded to a multiple of 256)
+  uint16_t* mout;        // clip-mask bits: bit (row % 16) of word [row / 16][col] (nullable)
+  int64_t ldm;           // words per 16-row block of mout (>= kq)
+  float tau_coef;        // set by launch_grid: error-bound coefficient of the float32 delta
+  int nit;               // set by launch_grid: 16-row rounds per wave
 };
 
 // bf16 MFMA GEMM family.  C[M][N] = sum_K a(M, K) b(K, N) with the operand
@@ -39,8 +41,8 @@ struct GemmArgs {
   const float* sx;        // per-token activation scale [T] (W4A8) or null
   void* out;              // kFwd: Y [T][m]; kDx: dX [T][k]
   int64_t ldo;
-  const uint8_t* mask;    // kDw: transposed clip-mask bits [k][ldm]
-  int64_t ldm;
+  const uint16_t* mask;   // kDw: clip-mask bits, bit (row % 16) of word [row / 16][col]
+  int64_t ldm;            // words per 16-row block
   const float* Am;        // kDw: A [m][r]
   const float* Bm;        // kDw: B [r][k]
   int r;
@@ -81,8 +83,8 @@ struct F32Args {
   const float* dY;
   const uint8_t* q;       // packed q [m][ldq]
   int64_t ldq;
-  const uint8_t* mask;    // transposed clip-mask bits [k][ldm]
-  int64_t ldm;
+  const uint16_t* mask;   // clip-mask bits, bit (row % 16) of word [row / 16][col]
+  int64_t ldm;            // words per 16-row block
   const float* s;
   int64_t gsize, ngroups;
   const float* A;
