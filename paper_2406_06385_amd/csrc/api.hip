@@ -361,10 +361,13 @@ lrqat_status lrqat_backward(const lrqat_layer* layer, int64_t tokens, const void
   p.dA_part = dA_part; p.dB_part = dB_part;
   LRQAT_TRY(hip_status(timed("gemm_dw", st, [&] { return launch_gemm(kDw, d.act, d.g != 0, p, st); }), "gemm_dw"));
   const int64_t ntn = (d.k + GEMM_BN - 1) / GEMM_BN, ntm = (d.m + GEMM_BM - 1) / GEMM_BM;
-  LRQAT_TRY(hip_status(timed("reduce", st, [&] { return launch_reduce(dA_part, ntn, d.m * d.r, dA, d.c, accumulate, st); }),
-                       "reduce"));
-  LRQAT_TRY(hip_status(timed("reduce", st, [&] { return launch_reduce(dB_part, ntm, d.r * d.k, dB, d.c, accumulate, st); }),
-                       "reduce"));
+  Reduce2Args ra{};
+  ra.part[0] = dA_part; ra.nparts[0] = ntn; ra.n[0] = d.m * d.r; ra.out[0] = dA;
+  ra.part[1] = dB_part; ra.nparts[1] = ntm; ra.n[1] = d.r * d.k; ra.out[1] = dB;
+  for (int i = 0; i < 2; ++i) ra.vec[i] = ra.n[i] % 4 == 0 && aligned(ra.out[i], 16);
+  ra.c = d.c;
+  ra.accumulate = accumulate;
+  LRQAT_TRY(hip_status(timed("reduce", st, [&] { return launch_reduce2(ra, st); }), "reduce"));
   return LRQAT_OK;
 }
 

@@ -15,6 +15,48 @@ __global__ __launch_bounds__(256) void k_reduce(const float* __restrict__ part, 
   out[idx] = (accumulate ? out[idx] : 0.f) + c * s;
 }
 
+// Both rank-r gradients in one launch: out = (accumulate ? out : 0) + c * sum_p part[p] for
+// dA (side 0) and dB (side 1).  Four consecutive elements per thread; the partial buffers
+// are summed in a fixed order (two interleaved running sums), so results are deterministic.
+__global__ __launch_bounds__(256) void k_reduce2(Reduce2Args ra) {
+  const int64_t t = int64_t(blockIdx.x) * 256 + threadIdx.x;
+  const int64_t nt0 = (ra.n[0] + 3) / 4;
+  const int side = t < nt0 ? 0 : 1;
+  const int64_t idx = 4 * (side ? t - nt0 : t);
+  const int64_t n = ra.n[side], np = ra.nparts[side];
+  if (idx >= n) return;
+  const float* part = ra.part[side] + idx;
+  float* out = ra.out[side] + idx;
+  if (ra.vec[side] && idx + 4 <= n) {
+    f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
+    int64_t q = 0;
+    for (; q + 2 <= np; q += 2) {
+      s0 += *reinterpret_cast<const f32x4*>(part + q * n);
+      s1 += *reinterpret_cast<const f32x4*>(part + (q + 1) * n);
+    }
+    if (q < np) s0 += *reinterpret_cast<const f32x4*>(part + q * n);
+    const f32x4 prev = ra.accumulate ? *reinterpret_cast<const f32x4*>(out) : f32x4{0.f, 0.f, 0.f, 0.f};
+    *reinterpret_cast<f32x4*>(out) = prev + ra.c * (s0 + s1);
+  } else {
+    for (int64_t e = 0; e < 4 && idx + e < n; ++e) {
+      float s0 = 0.f, s1 = 0.f;
+      int64_t q = 0;
+      for (; q + 2 <= np; q += 2) {
+        s0 += part[q * n + e];
+        s1 += part[(q + 1) * n + e];
+      }
+      if (q < np) s0 += part[q * n + e];
+      out[e] = (ra.accumulate ? out[e] : 0.f) + ra.c * (s0 + s1);
+    }
+  }
+}
+
+hipError_t launch_reduce2(const Reduce2Args& ra, hipStream_t st) {
+  const int64_t nt = (ra.n[0] + 3) / 4 + (ra.n[1] + 3) / 4;
+  k_reduce2<<<unsigned((nt + 255) / 256), 256, 0, st>>>(ra);
+  return hipGetLastError();
+}
+
 hipError_t launch_gemm(GemmVariant v, bool act, bool grouped, const GemmArgs& p, hipStream_t st) {
   switch (v) {
     case kFwd:

@@ -519,16 +519,18 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int64_t col = n0 + wn + 32 * j + (lane & 31);
-      mbits[j] = u32x4{0u, 0u, 0u, 0u};
-      if (col < p.N) {
-        const uint16_t* mp = p.mask + (rowb >> 4) * p.ldm + col;
+      // unconditional 2-byte buffer loads (no branch around a load); columns >= N are dropped
+      const auto rm = rsrc(p.mask + (rowb >> 4) * p.ldm, 8 * p.ldm * 2);
 #pragma unroll
-        for (int i = 0; i < 4; ++i) mbits[j][i] = uint32_t(mp[2 * i * p.ldm]) | (uint32_t(mp[(2 * i + 1) * p.ldm]) << 16);
+      for (int i = 0; i < 4; ++i) {
+        const uint32_t w = ld16(rm, uint32_t((2 * i * p.ldm + col) * 2)) |
+                           (ld16(rm, uint32_t(((2 * i + 1) * p.ldm + col) * 2)) << 16);
+        mbits[j][i] = col < p.N ? w : 0u;
       }
     }
+    const auto rsg = rsrc(p.s + m0 * p.ngroups, (p.M - m0) * p.ngroups * 4);  // group-wise scales of the block's rows
     if constexpr (!GRP) {
-      const int64_t row = m0 + threadIdx.x;
-      s_tile[threadIdx.x] = row < p.M ? p.s[row] : 0.f;
+      s_tile[threadIdx.x] = ldf(rsg, uint32_t(threadIdx.x * 4));  // rows >= M read 0
       __syncthreads();
     }
 #pragma unroll
@@ -550,7 +552,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
             // the padded mask region past row m is not written by the grid pass
             const bool in = (mbits[j][i] >> acc_row(v, lane)) & 1 && m0 + li < p.M && col < p.N;
             float sc;
-            if constexpr (GRP) sc = in ? p.s[(m0 + li) * p.ngroups + col / p.gsize] : 0.f;
+            if constexpr (GRP) sc = ldf(rsg, uint32_t((li * p.ngroups + col / p.gsize) * 4));  // rows >= M read 0
             else sc = sc4[e];
             const float g = in ? acc[i][j][v] * sc : 0.f;
             Gs[g_off(li, lj)] = __builtin_bit_cast(uint16_t, (__bf16)g);
@@ -562,14 +564,22 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     auto stage = [&](const float* __restrict__ src, bool is_a, int rb) {
       const int rho_l = threadIdx.x >> 3, c0 = 32 * (threadIdx.x & 7);
       const int rho = 32 * rb + rho_l;
+      // unconditional buffer loads, all in flight at once: rows of A past M and ranks of B past r
+      // lie outside the resource and read 0; ranks of A past r and columns of B past N are zeroed
+      const auto rs = is_a ? rsrc(src + m0 * r, (p.M - m0) * int64_t(r) * 4) : rsrc(src + n0, (int64_t(r) * p.N - n0) * 4);
+      float xv[32];
+#pragma unroll
+      for (int i = 0; i < 32; ++i) {
+        const int c = c0 + i;
+        xv[i] = ldf(rs, is_a ? uint32_t((c * r + rho) * 4) : uint32_t((int64_t(rho) * p.N + c) * 4));
+      }
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         float x[8];
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
           const int c = c0 + 8 * q + e;
-          if (is_a) x[e] = (rho < r && m0 + c < p.M) ? src[(m0 + c) * r + rho] : 0.f;   // A[m0 + c][rho]
-          else x[e] = (rho < r && n0 + c < p.N) ? src[int64_t(rho) * p.N + n0 + c] : 0.f;  // B[rho][n0 + c]
+          x[e] = (rho < r && (is_a || n0 + c < p.N)) ? xv[8 * q + e] : 0.f;  // A[m0 + c][rho] or B[rho][n0 + c]
         }
         u32x4 o;
 #pragma unroll

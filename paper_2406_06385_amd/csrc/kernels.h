@@ -73,6 +73,15 @@ hipError_t launch_dw_act(const GemmArgs& p, hipStream_t st);
 hipError_t launch_dw_act_grp(const GemmArgs& p, hipStream_t st);
 hipError_t launch_reduce(const float* part, int64_t nparts, int64_t n, float* out, float c, int accumulate,
                          hipStream_t st);
+struct Reduce2Args {        // side 0: dA, side 1: dB
+  const float* part[2];     // [nparts][n] partial sums
+  int64_t nparts[2], n[2];
+  float* out[2];
+  int vec[2];               // 16-byte aligned rows and n % 4 == 0
+  float c;
+  int accumulate;
+};
+hipError_t launch_reduce2(const Reduce2Args& ra, hipStream_t st);
 
 // float32 activation path (simple tiled FMA kernels).
 struct F32Args {
