@@ -68,22 +68,34 @@ def kernel_flops(name, wl, spec):
             "grid": 2.0 * m * k * r}.get(name)
 
 
+# Sources each library kernel is compiled from: a traffic record stays valid
+# while these files are unchanged.
+KERNEL_SOURCES = {
+    "gemm_fwd": ["gemm_impl.h", "gemm_fwd.hip", "kernels.h", "common.h"],
+    "gemm_dx": ["gemm_impl.h", "gemm_dx.hip", "kernels.h", "common.h"],
+    "gemm_dw": ["gemm_impl.h", "gemm_dw.hip", "kernels.h", "common.h"],
+    "grid": ["grid.hip", "kernels.h", "common.h"],
+    "reduce": ["gemm.hip", "kernels.h", "common.h"],
+}
+
+
 def traffic_record(kernel):
     """HBM bytes per launch measured with rocprofv3 counters, if the kernel's
     sources are unchanged since the measurement (else None)."""
     path = os.path.join(ROOT, "profiles", f"traffic_{kernel}.json")
-    if not os.path.exists(path):
+    if not os.path.exists(path) or kernel not in KERNEL_SOURCES:
         return None
     rec = json.load(open(path))
-    if rec.get("sources_sha256") != sources_sha():
+    if rec.get("sources_sha256") != sources_sha(kernel):
         return None
     return rec.get("hbm_bytes_per_launch")
 
 
-def sources_sha():
+def sources_sha(kernel):
+    """sha256 over the kernel's source files (names and contents)."""
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2406_06385_amd", "csrc")
-    for f in sorted(os.listdir(csrc)):
+    for f in sorted(KERNEL_SOURCES[kernel]):
         h.update(f.encode())
         h.update(open(os.path.join(csrc, f), "rb").read())
     return h.hexdigest()
