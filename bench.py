@@ -74,7 +74,7 @@ KERNEL_SOURCES = {
     "gemm_fwd": ["gemm_impl.h", "gemm_fwd.hip", "kernels.h", "common.h"],
     "gemm_dx": ["gemm_impl.h", "gemm_dx.hip", "kernels.h", "common.h"],
     "gemm_dw": ["gemm_impl.h", "gemm_dw.hip", "kernels.h", "common.h"],
-    "grid": ["grid.hip", "kernels.h", "common.h"],
+    "grid": ["grid.hip", "grid_swar.h", "kernels.h", "common.h"],
     "reduce": ["gemm.hip", "kernels.h", "common.h"],
 }
 

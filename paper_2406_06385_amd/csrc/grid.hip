@@ -6,6 +6,7 @@
 //     the per-call reconstruction pass of the forward/backward and the merge
 //     for inference (W_Z);
 //   * per-token int8 activation quantisation (Section 4, W4A8).
+#include "grid_swar.h"
 #include "kernels.h"
 
 namespace lrqat {
@@ -205,6 +206,18 @@ __device__ __forceinline__ void load_b(float (&y)[8], const GridArgs& a, int64_t
   }
 }
 
+// Bytes 0..3 of the result: bit 7 is the sign of x[0..3].
+__device__ __forceinline__ uint32_t sign_bytes(const f32x4& x) {
+  const uint32_t lo = __builtin_amdgcn_perm(__float_as_uint(x[1]), __float_as_uint(x[0]), 0x0c0c0703u);
+  const uint32_t hi = __builtin_amdgcn_perm(__float_as_uint(x[3]), __float_as_uint(x[2]), 0x07030c0cu);
+  return lo | hi;
+}
+
+// Two words of four nibble-bytes each -> one word of eight nibbles (element 0 lowest).
+__device__ __forceinline__ uint32_t pack_nibble_bytes(uint32_t q0, uint32_t q1) {
+  return __builtin_amdgcn_perm(q1 | (q1 >> 4), q0 | (q0 >> 4), 0x06040200u);
+}
+
 // Rounding decision, clip, packing and mask of one 16 x 64 wave tile.
 //
 // Fast path: with Phi0 = n + cf 2^-f (n = floor, cf the f fraction bits),
@@ -227,7 +240,49 @@ __device__ __forceinline__ void grid_finish(const GridArgs& a, const PhiRegs& P,
   auto n_of = [&](int idx) { return PACKED ? phi_code<true>(P, idx) : phi_code<false>(P, idx) >> f; };
 
   int ut[16];
-  if (zero_delta) {
+  uint32_t w0 = 0, w1 = 0;
+  uint64_t mbal = 0;
+  bool done = false;  // q words (and an all-ones mask) already formed by the byte-parallel path
+  if (!zero_delta) {
+    // the regime of the byte-parallel path: every |delta| below the distance of the non-tie
+    // codes to their rounding points and above the error bound (so its sign is certain)
+    const float tz = fmaxf(tau, 0.f);
+    float amx = 0.f, amn = __builtin_inff();
+#pragma unroll
+    for (int cb = 0; cb < 4; ++cb)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        amx = fmaxf(amx, fabsf(acc[cb][v]));
+        amn = fminf(amn, fabsf(acc[cb][v]));
+      }
+    const float ac = fabsf(a.c);
+    const float lim = (PACKED ? 0.5f : __builtin_bit_cast(float, uint32_t(127 - f) << 23)) - tz - 0x1p-22f;
+    const bool fast = amx * ac < lim && amn * ac > tz && a.c != 0.f && (!PACKED || a.bits == 4);
+    if (!__builtin_amdgcn_ballot_w64(!fast)) {
+      if constexpr (PACKED) {
+        // |delta| < 1/2: q is Phi0 itself (INT4 codes are always on the grid)
+        w0 = P.w[0];
+        w1 = P.w[1];
+        done = true;
+      } else {
+        uint32_t q[4], clip = 0;
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const uint32_t sb = sign_bytes(acc[g]);
+          const uint32_t incb = ((a.c > 0.f ? ~sb : sb) >> 7) & 0x01010101u;
+          q[g] = swar_grid_q8(P.w[g], incb, f, a.bits, clip);
+        }
+        if (!__builtin_amdgcn_ballot_w64(clip != 0)) {
+          w0 = pack_nibble_bytes(q[0], q[1]);
+          w1 = pack_nibble_bytes(q[2], q[3]);
+          done = true;
+        }
+      }
+      mbal = ~uint64_t(0);
+    }
+  }
+  if (done) {
+  } else if (zero_delta) {
     // round-half-even of Phi0 = n + cf 2^-f
     const int half = f ? 1 << (f - 1) : 0;
 #pragma unroll
@@ -291,17 +346,17 @@ __device__ __forceinline__ void grid_finish(const GridArgs& a, const PhiRegs& P,
   // Clip and pack 16 nibbles (8 bytes; columns >= k are written as 0).  Mask:
   // lane L writes the 16-row word of tile column L = 16 (L / 16) + idx,
   // idx = L % 16, which is bits 16 (L / 16) .. +15 of the ballot of element idx.
-  uint32_t w0 = 0, w1 = 0;
-  uint64_t mbal = 0;
+  if (!done) {
 #pragma unroll
-  for (int idx = 0; idx < 16; ++idx) {
-    const int q = min(max(ut[idx], lo), hi);
-    const uint32_t nib = uint32_t(q & 15) << (4 * (idx & 7));
-    if (idx < 8) w0 |= nib;
-    else w1 |= nib;
-    if constexpr (MASK) {
-      const uint64_t bal = __builtin_amdgcn_ballot_w64(q == ut[idx]);
-      mbal = (lane & 15) == idx ? bal : mbal;
+    for (int idx = 0; idx < 16; ++idx) {
+      const int q = min(max(ut[idx], lo), hi);
+      const uint32_t nib = uint32_t(q & 15) << (4 * (idx & 7));
+      if (idx < 8) w0 |= nib;
+      else w1 |= nib;
+      if constexpr (MASK) {
+        const uint64_t bal = __builtin_amdgcn_ballot_w64(q == ut[idx]);
+        mbal = (lane & 15) == idx ? bal : mbal;
+      }
     }
   }
   if (kin < 16) {
