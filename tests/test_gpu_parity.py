@@ -296,6 +296,24 @@ def test_exact_ties_zero_and_tiny_b(lr):
             check_full(lr, c)
 
 
+def test_full_code_range_clips_in_the_byte_parallel_regime(lr):
+    """Phi0 codes drawn over the whole int8 range (not from the encoder), with a small
+    B: nearly every wave tile is in the regime of the byte-parallel decision but
+    holds codes n = hi with a fraction above one half, which round up off the grid.
+    Those must be clipped (mask 0), so the grid pass falls back to the exact path;
+    grid, merge bytes and the masked gradients must match the oracle."""
+    rng = np.random.default_rng(31)
+    for bits in (4, 3):
+        _log(f"[full code range q8 b{bits}]")
+        c = Case(lr, 320, 264, 96, 16, 16.0, bits, "q8", 0, 0, "bf16", seed=33)
+        c.phi0_ref = rng.integers(-128, 128, size=c.phi0_ref.shape).astype(np.int8)
+        c.d_phi0 = torch.from_numpy(c.phi0_ref).cuda()
+        _, M, _, _ = O.grid_from_inputs(c.phi0_ref, c.A, c.B, c.L.alpha, c.L.rank, bits, "q8")
+        assert (~M).sum() > 100, "the case should clip"
+        check_merge(lr, c)
+        check_full(lr, c)
+
+
 def test_accumulate_and_determinism(lr):
     c = Case(lr, 512, 512, 256, 32, 32.0, 4, "q8", 0, 0, "bf16", seed=3)
     check_full(lr, c, accumulate=True)
