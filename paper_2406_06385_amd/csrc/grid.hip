@@ -80,7 +80,7 @@ __global__ __launch_bounds__(256) void k_encode(const float* __restrict__ W0, co
 // near n = 0 it is exact.  Elements inside that bound are decided again from
 // a float64 delta, so the grid equals the exact one except within float64
 // rounding of a .5 point.
-constexpr int GR_COLS = 64, GR_THREADS = 256, GR_MIN_BLOCKS = 2048;
+constexpr int GR_COLS = 64, GR_THREADS = 256, GR_MIN_BLOCKS = 512;
 
 // 16x16x32 MFMA, D(16x16, f32) += P(16x32, bf16) Q(32x16, bf16): lane l
 // supplies row l % 16 of P and column l % 16 of Q, each with the 8 K-values
@@ -229,12 +229,13 @@ __device__ __forceinline__ uint32_t pack_nibble_bytes(uint32_t q0, uint32_t q1) 
 // margins and float64 deltas (rare).  Where delta is identically zero on the
 // strip (B = 0, the adapters' initial state) the grid is round-half-even of
 // Phi0, decided in integers.
-template <bool PACKED, bool MASK>
+template <bool PACKED, bool MASK, bool B4>
 __device__ __forceinline__ void grid_finish(const GridArgs& a, const PhiRegs& P, const f32x4 (&acc)[4], float tau,
                                             bool zero_delta, int64_t row, int64_t c16, int64_t rowblk, int64_t col0) {
   const int lane = threadIdx.x & 63;
-  const int lo = -(1 << (a.bits - 1)), hi = (1 << (a.bits - 1)) - 1;
-  const int f = PACKED ? 0 : 8 - a.bits;
+  const int bits = B4 ? 4 : a.bits;  // B4: the common 4-bit grid, constant for the compiler
+  const int lo = -(1 << (bits - 1)), hi = (1 << (bits - 1)) - 1;
+  const int f = PACKED ? 0 : 8 - bits;
   const bool row_ok = row < a.m;
   const int kin = int(max<int64_t>(0, min<int64_t>(16, a.k - c16)));  // the lane's columns inside k
   auto n_of = [&](int idx) { return PACKED ? phi_code<true>(P, idx) : phi_code<false>(P, idx) >> f; };
@@ -257,7 +258,7 @@ __device__ __forceinline__ void grid_finish(const GridArgs& a, const PhiRegs& P,
       }
     const float ac = fabsf(a.c);
     const float lim = (PACKED ? 0.5f : __builtin_bit_cast(float, uint32_t(127 - f) << 23)) - tz - 0x1p-22f;
-    const bool fast = amx * ac < lim && amn * ac > tz && a.c != 0.f && (!PACKED || a.bits == 4);
+    const bool fast = amx * ac < lim && amn * ac > tz && a.c != 0.f && (!PACKED || bits == 4);
     if (!__builtin_amdgcn_ballot_w64(!fast)) {
       if constexpr (PACKED) {
         // |delta| < 1/2: q is Phi0 itself (INT4 codes are always on the grid)
@@ -270,7 +271,7 @@ __device__ __forceinline__ void grid_finish(const GridArgs& a, const PhiRegs& P,
         for (int g = 0; g < 4; ++g) {
           const uint32_t sb = sign_bytes(acc[g]);
           const uint32_t incb = ((a.c > 0.f ? ~sb : sb) >> 7) & 0x01010101u;
-          q[g] = swar_grid_q8(P.w[g], incb, f, a.bits, clip);
+          q[g] = swar_grid_q8(P.w[g], incb, f, bits, clip);
         }
         if (!__builtin_amdgcn_ballot_w64(clip != 0)) {
           w0 = pack_nibble_bytes(q[0], q[1]);
@@ -382,7 +383,7 @@ __device__ __forceinline__ void grid_finish(const GridArgs& a, const PhiRegs& P,
 // COAL (r = 32, 16-byte aligned A and B rows, k % 4 == 0): B and A are read
 // with coalesced 16-byte loads and rearranged into MFMA operand order in the
 // wave's LDS region; otherwise each lane loads its own operand values.
-template <bool PACKED, bool ONEK, bool MASK, bool COAL>
+template <bool PACKED, bool ONEK, bool MASK, bool COAL, bool B4>
 __global__ __launch_bounds__(GR_THREADS) void k_grid(GridArgs a) {
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x >> 6));
@@ -570,7 +571,7 @@ __global__ __launch_bounds__(GR_THREADS) void k_grid(GridArgs a) {
     // -1 where delta is exactly zero (a zero A row or zero B columns, e.g. B at its zero
     // initialisation), so that no element is re-decided there
     const float tau = amx == 0.f ? -1.f : a.tau_coef * norm_bound(ass, amx, a.r) * nb;
-    grid_finish<PACKED, MASK>(a, Pc, acc, tau, bmx == 0.f, row, c16, rowblk, col0);
+    grid_finish<PACKED, MASK, B4>(a, Pc, acc, tau, bmx == 0.f, row, c16, rowblk, col0);
   }
 }
 
@@ -628,10 +629,15 @@ hipError_t launch_grid(const GridArgs& a0, hipStream_t st) {
   const unsigned nb = unsigned(nblocks);
   const bool coal = a.r == 32 && a.k % 4 == 0 && (reinterpret_cast<uintptr_t>(a.A) & 15) == 0 &&
                     (reinterpret_cast<uintptr_t>(a.B) & 15) == 0;
+  // 4-bit grids (the common W4 case) get an instantiation with the width fixed
   const int sel = (a.packed ? 8 : 0) | (a.r <= 32 ? 4 : 0) | (coal ? 2 : 0) | (a.mout ? 1 : 0);
+  const bool b4 = a.bits == 4;
   switch (sel) {
-#define LRQAT_GRID_CASE(S, P, O, C, M) \
-  case S: k_grid<P, O, M, C><<<nb, GR_THREADS, 0, st>>>(a); break;
+#define LRQAT_GRID_CASE(S, P, O, C, M)                                      \
+  case S:                                                                   \
+    if (b4) k_grid<P, O, M, C, true><<<nb, GR_THREADS, 0, st>>>(a);         \
+    else k_grid<P, O, M, C, false><<<nb, GR_THREADS, 0, st>>>(a);           \
+    break;
     LRQAT_GRID_CASE(0, false, false, false, false)
     LRQAT_GRID_CASE(1, false, false, false, true)
     LRQAT_GRID_CASE(4, false, true, false, false)
