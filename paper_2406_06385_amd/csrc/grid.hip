@@ -258,8 +258,32 @@ __device__ __forceinline__ void grid_finish(const GridArgs& a, const PhiRegs& P,
       }
     const float ac = fabsf(a.c);
     const float lim = (PACKED ? 0.5f : __builtin_bit_cast(float, uint32_t(127 - f) << 23)) - tz - 0x1p-22f;
-    const bool fast = amx * ac < lim && amn * ac > tz && a.c != 0.f && (!PACKED || bits == 4);
-    if (!__builtin_amdgcn_ballot_w64(!fast)) {
+    // INT4 codes have no ties: inside the regime q does not depend on delta at all
+    const bool fast = amx * ac < lim && (PACKED || amn * ac > tz) && a.c != 0.f && (!PACKED || bits == 4);
+    bool regime = amx * ac < lim && a.c != 0.f && (!PACKED || bits == 4);
+    if constexpr (!PACKED) {
+      // A wave whose smallest |delta| is within the bound may still be decidable: only ties
+      // (cf = 2^(f-1)) depend on delta, so check ties against the bound element by element.
+      if (__builtin_amdgcn_ballot_w64(!fast) && !__builtin_amdgcn_ballot_w64(!regime)) {
+        const uint32_t ones = 0x01010101u;
+        // covers the rounding of c * acc; never 0, so that a tie with delta exactly 0 is caught
+        const float tzu = fmaxf(tz * (1.f + 0x1p-20f), 0x1p-100f);
+        uint32_t bad = 0;
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          f32x4 d;
+#pragma unroll
+          for (int v = 0; v < 4; ++v) d[v] = __builtin_fmaf(fabsf(acc[g][v]), ac, -tzu);  // < 0: within the bound
+          const uint32_t y = (P.w[g] & (ones * ((1u << f) - 1))) ^ (ones << (f - 1));  // 0 in tie bytes
+          const uint32_t tie = ~((y + 0x7F7F7F7Fu) | y) & 0x80808080u;
+          bad |= sign_bytes(d) & tie;
+        }
+        regime = bad == 0;
+      } else {
+        regime = fast;
+      }
+    }
+    if (!__builtin_amdgcn_ballot_w64(!(PACKED ? fast : regime))) {
       if constexpr (PACKED) {
         // |delta| < 1/2: q is Phi0 itself (INT4 codes are always on the grid)
         w0 = P.w[0];
