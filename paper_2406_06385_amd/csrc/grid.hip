@@ -59,9 +59,10 @@ __global__ __launch_bounds__(256) void k_encode(const float* __restrict__ W0, co
 }
 
 // ============================================================================ grid
-// A block owns a strip of 64 columns and 64 * nit rows; in round it
-// (0 .. nit-1) wave w handles the 16-row block 4 it + w.  For a 16 x 64 wave
-// tile, delta = c A B comes from 16x16x32 MFMAs on bfloat16 hi/lo splits,
+// A block owns 256 adjacent columns and nit consecutive 16-row blocks; wave w
+// takes columns 64 w .. 64 w + 63 of the block and walks its nit row blocks
+// (prefetching the next one).  For a 16 x 64 wave tile, delta = c A B comes
+// from 16x16x32 MFMAs on bfloat16 hi/lo splits,
 // A B ~ Ahi Bhi + Ahi Blo + Alo Bhi, accumulated in float32.  The product is
 // transposed (B columns are the MFMA row operand) and the B columns of column
 // block cb (0..3) are permuted: MFMA row i stands for column
@@ -218,17 +219,20 @@ __device__ __forceinline__ uint32_t pack_nibble_bytes(uint32_t q0, uint32_t q1) 
   return __builtin_amdgcn_perm(q1 | (q1 >> 4), q0 | (q0 >> 4), 0x06040200u);
 }
 
-// Rounding decision, clip, packing and mask of one 16 x 64 wave tile.
-//
-// Fast path: with Phi0 = n + cf 2^-f (n = floor, cf the f fraction bits),
-// u = n + 1/2 + w and w = (cf 2^-f - 1/2) + delta, evaluated as one fused
-// multiply-add from exact terms.  For w in (-1, 1) and w != 0 the nearest
-// integer to u is n + [w > 0].  The answer is certain unless |w| lies within
-// the error bound tau of 0, or |w| is at least 1 - tau (a decision point at
-// +-1, or beyond); a wave with such an element redoes its tile with exact
-// margins and float64 deltas (rare).  Where delta is identically zero on the
-// strip (B = 0, the adapters' initial state) the grid is round-half-even of
-// Phi0, decided in integers.
+// Rounding decision, clip, packing and mask of one 16 x 64 wave tile, by the
+// cheapest of three paths that is exact for the whole wave:
+//  * delta identically zero on the strip (B = 0, the adapters' initial
+//    state): round-half-even of Phi0, decided in integers;
+//  * byte-parallel (swar_grid_q8): every |delta| is below the distance of the
+//    non-tie codes to their rounding points and, at ties, above the error bound
+//    tau, so only a tie depends on delta, through its sign; INT4 Phi0 is then q
+//    itself.  Codes that would round off the grid send the wave on;
+//  * per element: with Phi0 = n + cf 2^-f (n = floor, cf the f fraction bits),
+//    u = n + 1/2 + w and w = (cf 2^-f - 1/2) + delta, one fused multiply-add of
+//    exact terms; for w in (-1, 1), w != 0, the nearest integer to u is
+//    n + [w > 0].  That is certain unless |w| lies within tau of 0 or is at
+//    least 1 - tau; a wave with such an element redoes its tile with exact
+//    margins and float64 deltas (rare).
 template <bool PACKED, bool MASK, bool B4>
 __device__ __forceinline__ void grid_finish(const GridArgs& a, const PhiRegs& P, const f32x4 (&acc)[4], float tau,
                                             bool zero_delta, int64_t row, int64_t c16, int64_t rowblk, int64_t col0) {
