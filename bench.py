@@ -42,6 +42,8 @@ def parse():
     ap.add_argument("--workload", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU time of the oracle sample")
+    ap.add_argument("--vendor-gemm", action="store_true",
+                    help="only time the vendor library's plain bf16 GEMMs of the layer's three shapes and exit")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB (calibrates rocprofv3 byte counters) and exit")
     return ap.parse_args()
@@ -57,6 +59,31 @@ def copy_probe(mib):
         dst.copy_(src)
     torch.cuda.synchronize()
     print(json.dumps({"copy_probe_bytes_read": n * 4, "copy_probe_bytes_written": n * 4}), flush=True)
+
+
+def vendor_gemm(wl):
+    """Context, not part of the path: torch.matmul (hipBLASLt) on plain bf16 GEMMs of the same three
+    shapes as the layer's forward (X W^T), dX (dY W) and dW (dY^T X), with no quantisation work."""
+    import torch
+    spec = wl.layers[0]
+    T, m, k = wl.tokens, spec.m, spec.k
+    X = torch.randn(T, k, dtype=torch.bfloat16, device="cuda")
+    W = torch.randn(m, k, dtype=torch.bfloat16, device="cuda")
+    dY = torch.randn(T, m, dtype=torch.bfloat16, device="cuda")
+    out = {}
+    for name, fn in (("fwd_X_Wt", lambda: X @ W.t()), ("dx_dY_W", lambda: dY @ W), ("dw_dYt_X", lambda: dY.t() @ X)):
+        for _ in range(5):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(20):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        us = 1e3 * e0.elapsed_time(e1) / 20
+        out[name] = {"us": us, "TFLOP/s": 2.0 * T * m * k / (us * 1e-6) / 1e12}
+    print(json.dumps({"vendor_gemm": out, "workload": wl.name}), flush=True)
 
 
 def kernel_flops(name, wl, spec):
@@ -143,6 +170,10 @@ def main():
     args = parse()
     if args.copy_probe:
         copy_probe(args.copy_probe)
+        return
+    if args.vendor_gemm:
+        from paper_2406_06385_amd import inputs as I
+        vendor_gemm(I.WORKLOADS[args.workload])
         return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the multi-GPU path is not part "
