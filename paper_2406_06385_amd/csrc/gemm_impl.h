@@ -357,6 +357,30 @@ struct Loader<kDw, ACT, GRP, VEC> {
 // different chunk slots.
 __device__ __forceinline__ int g_off(int i, int j) { return i * 256 + ((((j >> 3) ^ (i & 31))) << 3) + (j & 7); }
 
+// LDS transpose load (gfx950): lane i of each 16-lane group receives the 4
+// values in column i % 4 of the 4-element rows that lanes 4 e + i / 4 address
+// (e = 0..3).
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ u32x2 ld_tr16(const uint16_t* p) {
+  const s16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) s16x4*)(const_cast<uint16_t*>(p)));
+  return __builtin_bit_cast(u32x2, v);
+}
+
+// MFMA operand from a [K][256] staging tile laid out by g_off: lane l gets
+// column c0 + l % 32 at the 8 K rows k0 + 8 (l / 32) .. +7.  Lanes 4 e + q of
+// each 16-lane group point at K row k0 + 8 (l / 32) + e (+4 for the second
+// half) and columns c0 + 16 ((l / 16) % 2) + 4 q, so lane i of the group
+// receives column c0 + 16 ((l / 16) % 2) + i.
+__device__ __forceinline__ u32x4 frag_tr_g(const uint16_t* tile, int c0, int k0, int lane) {
+  const int g = lane >> 4, r = lane & 15;
+  const int c = c0 + 16 * (g & 1) + 4 * (r & 3);
+  const int k = k0 + 8 * (g >> 1) + (r >> 2);
+  const u32x2 lo = ld_tr16(tile + g_off(k, c));
+  const u32x2 hi = ld_tr16(tile + g_off(k + 4, c));
+  return u32x4{lo[0], lo[1], hi[0], hi[1]};
+}
+
 // Instruction interleave of one K-tile (one scheduling region): the first
 // k-step's fragment reads, then each MFMA followed by a few VALU ops of the
 // next tile's conversion; the fragment reads of the following k-step ride on
@@ -504,8 +528,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
         }
     }
   } else {
-    // ---- dW epilogue: G = s * M * dW staged in LDS (bf16), then both rank-r
-    // products from LDS; the accumulators are dead once G is staged.
+    // ---- dW epilogue: G = s * M * dW staged in LDS (bf16, transposed), then both
+    // rank-r products from LDS; the accumulators are dead once G is staged.
     // Accumulator layout: acc[i][j][v] = dW[m0 + wm + 32 i + acc_row(v)][n0 + wn + 32 j + lane % 32].
     const int r = p.r;
     const int nrb = (r + 31) / 32;
@@ -545,6 +569,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
         for (int j = 0; j < 4; ++j) {
           const int lj = wn + 32 * j + (lane & 31);
           const int64_t col = n0 + lj;
+          float g[4];
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
             const int v = 4 * g4 + e;
@@ -554,9 +579,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
             float sc;
             if constexpr (GRP) sc = ldf(rsg, uint32_t((li * p.ngroups + col / p.gsize) * 4));  // rows >= M read 0
             else sc = sc4[e];
-            const float g = in ? acc[i][j][v] * sc : 0.f;
-            Gs[g_off(li, lj)] = __builtin_bit_cast(uint16_t, (__bf16)g);
+            g[e] = in ? acc[i][j][v] * sc : 0.f;
           }
+          // G is staged transposed, Gs[j][i]: the lane's 4 consecutive rows are one 8-byte write
+          *reinterpret_cast<u32x2*>(Gs + g_off(lj, lr)) = u32x2{pack_bf16x2(g[0], g[1]), pack_bf16x2(g[2], g[3])};
         }
       }
 
@@ -596,7 +622,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
       __syncthreads();  // G staged / previous rank block consumed
       stage(p.Am, true, rb);
       __syncthreads();
-      // dB: A operand = A^T rows (rt_tile), B operand = 8 consecutive rows of a G column
+      // dB: A operand = A^T rows (rt_tile), B operand = 8 consecutive rows of a G column (one read)
 #pragma unroll
       for (int cb2 = 0; cb2 < 2; ++cb2) {
         const int cb = 2 * wave + cb2;            // column block of 32
@@ -608,10 +634,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
         for (int s2 = 0; s2 < 16; ++s2) {
           const int ib = 16 * s2 + 8 * half;
           const u32x4 aa = *reinterpret_cast<const u32x4*>(&rt_tile[g_off(lane & 31, ib)]);
-          u32x4 gb;
-#pragma unroll
-          for (int q = 0; q < 4; ++q)
-            gb[q] = uint32_t(Gs[g_off(ib + 2 * q, lj)]) | (uint32_t(Gs[g_off(ib + 2 * q + 1, lj)]) << 16);
+          const u32x4 gb = *reinterpret_cast<const u32x4*>(Gs + g_off(lj, ib));  // G[ib .. ib + 7][lj]
           d = mfma32(aa, gb, d);
         }
         if (n0 + lj < p.N) {
@@ -626,7 +649,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
       __syncthreads();
       stage(p.Bm, false, rb);
       __syncthreads();
-      // dA: A operand = G rows, B operand = B rows (rt_tile)
+      // dA: A operand = G rows (transpose loads), B operand = B rows (rt_tile)
 #pragma unroll
       for (int h2 = 0; h2 < 2; ++h2) {
         const int rowblk = 2 * wave + h2;
@@ -635,8 +658,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
         for (int v = 0; v < 16; ++v) d[v] = 0.f;
 #pragma unroll 4
         for (int s2 = 0; s2 < 16; ++s2) {
-          const int li = 32 * rowblk + (lane & 31);
-          const u32x4 ga = *reinterpret_cast<const u32x4*>(Gs + g_off(li, 16 * s2 + 8 * half));
+          const u32x4 ga = frag_tr_g(Gs, 32 * rowblk, 16 * s2, lane);  // G[32 rowblk + l % 32][16 s2 + 8 half .. +7]
           const u32x4 bb = *reinterpret_cast<const u32x4*>(&rt_tile[g_off(lane & 31, 16 * s2 + 8 * half)]);
           d = mfma32(ga, bb, d);
         }
