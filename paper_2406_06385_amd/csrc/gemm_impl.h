@@ -565,21 +565,23 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
         const int lr = wm + 32 * i + 8 * g4 + 4 * half;
         f32x4 sc4 = {0.f, 0.f, 0.f, 0.f};
         if constexpr (!GRP) sc4 = *reinterpret_cast<const f32x4*>(&s_tile[lr]);
+        // rows lr .. lr + 3 inside M (the padded mask rows past m are not written by the grid pass)
+        const int64_t rows_in = p.M - m0 - lr;
+        const uint32_t rowbits = rows_in >= 4 ? 15u : rows_in <= 0 ? 0u : (1u << rows_in) - 1u;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           const int lj = wn + 32 * j + (lane & 31);
           const int64_t col = n0 + lj;
+          // the 4 rows' clip-mask bits (acc_row of element 4 g4 + e is 8 g4 + 4 half + e);
+          // columns past N have a zero mask word
+          const uint32_t bits = (mbits[j][i] >> (8 * g4 + 4 * half)) & rowbits;
           float g[4];
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
-            const int v = 4 * g4 + e;
-            const int li = lr + e;
-            // the padded mask region past row m is not written by the grid pass
-            const bool in = (mbits[j][i] >> acc_row(v, lane)) & 1 && m0 + li < p.M && col < p.N;
             float sc;
-            if constexpr (GRP) sc = ldf(rsg, uint32_t((li * p.ngroups + col / p.gsize) * 4));  // rows >= M read 0
+            if constexpr (GRP) sc = ldf(rsg, uint32_t(((lr + e) * p.ngroups + col / p.gsize) * 4));  // rows >= M read 0
             else sc = sc4[e];
-            g[e] = in ? acc[i][j][v] * sc : 0.f;
+            g[e] = (bits >> e) & 1u ? acc[i][j][4 * g4 + e] * sc : 0.f;
           }
           // G is staged transposed, Gs[j][i]: the lane's 4 consecutive rows are one 8-byte write
           *reinterpret_cast<u32x2*>(Gs + g_off(lj, lr)) = u32x2{pack_bf16x2(g[0], g[1]), pack_bf16x2(g[2], g[3])};
