@@ -86,6 +86,21 @@ def test_grid_golden(line):
     assert bool(M[0, 0]) == bool(int(m_want))
 
 
+@pytest.mark.parametrize("line", list(_rows("near.txt")))
+def test_near_window_golden(line):
+    fmt, bits, stored, delta, near_want = line.split()
+    bits, stored, delta = int(bits), int(stored), float(delta)
+    if fmt == O.FMT_Q8:
+        phi0 = np.array([[stored]], np.int8)
+        B = np.array([[1.0]], np.float32)
+    else:
+        phi0 = O.pack_int4(np.array([[stored, 0]]))
+        B = np.array([[1.0, 0.0]], np.float32)
+    A = np.array([[delta]], np.float32)
+    _, _, near, _ = O.grid_from_inputs(phi0, A, B, 1.0, 1, bits, fmt)
+    assert bool(near[0, 0]) == bool(int(near_want))
+
+
 @pytest.mark.parametrize("line", list(_rows("pack_int4.txt")))
 def test_pack_golden(line):
     vals, byts = [p.strip() for p in line.split(";")]
@@ -267,6 +282,82 @@ def test_exact_rational_brute_force(fmt, bits, g):
     gr = O.backward(L, X, phi0, s, A, B, dY)
     assert q.tolist() == q_b and M.astype(int).tolist() == M_b
     assert _close(Y_b, Y) and _close(dX_b, gr["dX"]) and _close(dA_b, gr["dA"]) and _close(dB_b, gr["dB"])
+
+
+def _f32_round(x: Fraction) -> Fraction:
+    """Nearest IEEE binary32 value of an exact rational (round half to even),
+    for normal magnitudes: 24 significant bits."""
+    if x == 0:
+        return Fraction(0)
+    sign = -1 if x < 0 else 1
+    a = abs(x)
+    e = math.floor(math.log2(a.numerator) - math.log2(a.denominator))
+    while Fraction(2) ** e > a:
+        e -= 1
+    while Fraction(2) ** (e + 1) <= a:
+        e += 1
+    ulp = Fraction(2) ** (e - 23)
+    return sign * _rne(a / ulp) * ulp
+
+
+def _act_quant_exact(X):
+    """Per-token symmetric int8 fake quantisation (Section 4 'Quantization',
+    Eq. dequant with z = 0 and b = 8) in exact rationals: s_x = fl32(max|X_t| / 127),
+    n = clip(round(fl32(X / s_x)), -128, 127), X_hat = s_x n; a zero row gives
+    X_hat = 0.  fl32 is the correctly rounded float32 value (the float32 scale and
+    quotient of the reading both sides take)."""
+    out = []
+    for row in X:
+        xs = [Fraction(float(v)) for v in row]
+        amax = max(abs(v) for v in xs)
+        sx = _f32_round(amax / 127)
+        if sx == 0:
+            out.append([Fraction(0)] * len(xs))
+            continue
+        out.append([sx * min(max(_rne(_f32_round(v / sx)), -128), 127) for v in xs])
+    return out
+
+
+@pytest.mark.parametrize("fmt,bits,g", [(O.FMT_PACKED, 4, 0), (O.FMT_Q8, 4, 3)])
+def test_exact_rational_brute_force_w4a8(fmt, bits, g):
+    """The W4A8 composition: the GEMMs see X_hat (not X, not the codes), dX passes
+    straight through the activation quantiser, dW = dY^T X_hat.  Token 1 is all
+    zeros; token 2 has s_x = 1/8 exactly and entries at exact ties X/s_x = n + 1/2."""
+    rng = np.random.default_rng(17)
+    m, k, r, T = 4, 6, 2, 4
+    lo, hi = O.grid_limits(bits)
+    f = 8 - bits
+    if fmt == O.FMT_Q8:
+        codes = rng.integers(-128, 128, size=(m, k))
+        phi0 = codes.astype(np.int8)
+        vals = [[Fraction(int(codes[i, j]), 1 << f) for j in range(k)] for i in range(m)]
+    else:
+        ints = rng.integers(lo, hi + 1, size=(m, k))
+        phi0 = O.pack_int4(ints)
+        vals = [[Fraction(int(ints[i, j])) for j in range(k)] for i in range(m)]
+    A = rng.normal(0, 0.4, size=(m, r)).astype(np.float32)
+    B = rng.normal(0, 0.4, size=(r, k)).astype(np.float32)
+    s = rng.uniform(0.5, 2.0, size=(m,) if g == 0 else (m, k // g)).astype(np.float32)
+    X = rng.normal(0, 3.0, size=(T, k)).astype(np.float32)
+    X[1, :] = 0.0
+    # 127/8 = 15.875 -> s_x = 0.125; 0.3125 / 0.125 = 2.5 and -0.6875 / 0.125 = -5.5 are ties
+    X[2, :] = [15.875, 0.3125, -0.6875, 1.0, -0.1875, 0.0625]
+    dY = rng.normal(size=(T, m)).astype(np.float32)
+    L = O.Layer(m, k, r, 1.5, bits, fmt, g, 8)
+    Xh = _act_quant_exact(X)
+    assert Xh[2][1] == Fraction(2, 8) and Xh[2][2] == Fraction(-6, 8) and Xh[2][4] == Fraction(-2, 8)
+    assert all(v == 0 for v in Xh[1])
+    Xh_f = np.array([[float(v) for v in row] for row in Xh])
+    # the brute force of the unquantised layer, fed X_hat, is the W4A8 layer
+    q_b, M_b, Y_b, dX_b, dA_b, dB_b = _brute(O.Layer(m, k, r, 1.5, bits, fmt, g, 0), Xh_f, vals, s, A, B, dY)
+    assert all(Fraction(float(v)) == w for rowv, roww in zip(Xh_f, Xh) for v, w in zip(rowv, roww))
+    Y, q, M, _ = O.forward(L, X, phi0, s, A, B)
+    gr = O.backward(L, X, phi0, s, A, B, dY)
+    assert q.tolist() == q_b and M.astype(int).tolist() == M_b
+    assert _close(Y_b, Y) and _close(dX_b, gr["dX"]) and _close(dA_b, gr["dA"]) and _close(dB_b, gr["dB"])
+    # the same layer without activation quantisation differs (the pin can see the quantiser)
+    Y0 = O.forward(O.Layer(m, k, r, 1.5, bits, fmt, g, 0), X, phi0, s, A, B)[0]
+    assert not np.allclose(Y0, Y, rtol=1e-6, atol=0)
 
 
 # ----------------------------------------------------------------------------- gradients
