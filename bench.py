@@ -2,12 +2,14 @@
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload 2] [--no-cpu-baseline]
 
-A step is lrqat_forward followed by lrqat_backward (dX, dA, dB) on one batch of
-seeded synthetic inputs already resident in device memory: the LLaMA-7B
-q_proj-shaped layer 4096 -> 4096 with 8 x 1024 tokens, rank 32, alpha 32, W4
-per-channel and Phi0 in fixed point Q4.4 by default.  Prints one JSON line.
+A step is lrqat_forward followed by lrqat_backward (dX, dA, dB) for every linear
+of the workload, each on its own batch of seeded synthetic inputs already
+resident in device memory.  The default workload is the LLaMA-7B q_proj-shaped
+layer 4096 -> 4096 with 8 x 1024 tokens, rank 32, alpha 32, W4 per-channel and
+Phi0 in fixed point Q4.4.  Prints one JSON line.
 
-value = algorithmic flops per step (6 T m k + 8 m k r) / step time, in TFLOP/s.
+value = algorithmic flops per step (sum over the layers of 6 T m k + 8 m k r)
+/ step time, in TFLOP/s.
 roofline: the kernel with the largest share of the step, timed with HIP events
 on the library's stream, against the bf16 dense MFMA peak of 2.5 PFLOP/s.
 cpu_baseline: the CPU oracle on a bounded token sample of the same layer.
@@ -18,6 +20,7 @@ layer holds (analytic, with checkpointing) beside torch's measured peak.
 from __future__ import annotations
 
 import argparse
+import dataclasses
 import hashlib
 import json
 import os
@@ -40,6 +43,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", type=int, default=2)
+    ap.add_argument("--rank", type=int, default=0, help="override the workload's rank r (and alpha = r)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU time of the oracle sample")
     ap.add_argument("--vendor-gemm", action="store_true",
@@ -86,13 +90,15 @@ def vendor_gemm(wl):
     print(json.dumps({"vendor_gemm": out, "workload": wl.name}), flush=True)
 
 
-def kernel_flops(name, wl, spec):
-    """Algorithmic flops of one launch of a library kernel (the useful work it does)."""
-    T, m, k, r = wl.tokens, spec.m, spec.k, wl.rank
-    return {"gemm_fwd": 2.0 * T * m * k,
-            "gemm_dx": 2.0 * T * m * k,
-            "gemm_dw": 2.0 * T * m * k + 4.0 * m * k * r,
-            "grid": 2.0 * m * k * r}.get(name)
+def kernel_flops(name, wl):
+    """Algorithmic flops of one step's launches of a library kernel (the useful
+    work they do), summed over the workload's layers."""
+    T, r = wl.tokens, wl.rank
+    per = {"gemm_fwd": lambda m, k: 2.0 * T * m * k,
+           "gemm_dx": lambda m, k: 2.0 * T * m * k,
+           "gemm_dw": lambda m, k: 2.0 * T * m * k + 4.0 * m * k * r,
+           "grid": lambda m, k: 2.0 * m * k * r}.get(name)
+    return None if per is None else sum(per(L.m, L.k) for L in wl.layers)
 
 
 # Sources each library kernel is compiled from: a traffic record stays valid
@@ -129,7 +135,7 @@ def sources_sha(kernel):
 
 
 def cpu_baseline(wl, inp, target_s):
-    """Oracle forward + backward on the first Ts tokens of the workload's layer."""
+    """Oracle forward + backward of the workload's first layer on its first Ts tokens."""
     from oracle import lrqat_oracle as O
     from paper_2406_06385_amd import inputs as I
     try:
@@ -160,10 +166,10 @@ def cpu_baseline(wl, inp, target_s):
     while total < target_s * 0.6 and reps < 64:
         total += run(ts)
         reps += 1
-    flops = wl.flops_fwd_bwd(ts) * reps
+    flops = (6.0 * ts * spec.m * spec.k + 8.0 * spec.m * spec.k * wl.rank) * reps
     return {"value": flops / total / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"float64 numpy oracle forward+backward of the same layer on its first {ts} of "
-                      f"{wl.tokens} tokens, {reps} run(s), {total:.1f} s"}
+            "sample": f"float64 numpy oracle forward+backward of layer {spec.name} ({spec.m}x{spec.k}) on its first "
+                      f"{ts} of {wl.tokens} tokens, {reps} run(s), {total:.1f} s"}
 
 
 def main():
@@ -187,12 +193,9 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     lrqat.load_library()
     wl = I.WORKLOADS[args.workload]
-    lspec = wl.layers[0]
-    T, m, k, r = wl.tokens, lspec.m, lspec.k, wl.rank
-    print(f"[bench] workload {wl.name}: generating inputs", file=sys.stderr, flush=True)
-    inp = I.make_layer_inputs(wl, 0)
-    spec = lrqat.LayerSpec(m, k, r, wl.alpha, wl.bits, wl.phi_format, wl.group_size, wl.act_bits, wl.act_dtype)
-
+    if args.rank:
+        wl = dataclasses.replace(wl, rank=args.rank, alpha=float(args.rank))
+    T, r = wl.tokens, wl.rank
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
 
@@ -201,24 +204,41 @@ def main():
             return torch.from_numpy(a.view(np.int16).copy()).view(torch.bfloat16).to(dev)
         return torch.from_numpy(a).to(dev)
 
-    W0 = torch.from_numpy(inp.W0).to(dev)
-    A = torch.from_numpy(inp.A).to(dev)
-    B = torch.from_numpy(inp.B).to(dev)
-    X = act(inp.X)
-    dY = act(inp.dY)
-    s0, phi0 = lrqat.lrqat_init_from_weights(spec, W0)
-    del W0
-    Y = torch.empty((T, m), dtype=spec.torch_dtype, device=dev)
-    dX = torch.empty((T, k), dtype=spec.torch_dtype, device=dev)
-    dA = torch.empty((m, r), dtype=torch.float32, device=dev)
-    dB = torch.empty((r, k), dtype=torch.float32, device=dev)
-    ws_f = lrqat.workspace(lrqat.lrqat_forward_workspace_size(spec, T), dev)
-    ws_b = lrqat.workspace(lrqat.lrqat_backward_workspace_size(spec, T), dev)
+    layers = []
+    inp0 = None
+    for li, lspec in enumerate(wl.layers):
+        print(f"[bench] workload {wl.name}: generating inputs of layer {lspec.name} ({lspec.m}x{lspec.k})",
+              file=sys.stderr, flush=True)
+        inp = I.make_layer_inputs(wl, li)
+        if li == 0:
+            inp0 = inp
+        m, k = lspec.m, lspec.k
+        spec = lrqat.LayerSpec(m, k, r, wl.alpha, wl.bits, wl.phi_format, wl.group_size, wl.act_bits, wl.act_dtype)
+        W0 = torch.from_numpy(inp.W0).to(dev)
+        s0, phi0 = lrqat.lrqat_init_from_weights(spec, W0)
+        torch.cuda.synchronize()
+        del W0
+        layers.append(dict(
+            spec=spec, s0=s0, phi0=phi0, A=torch.from_numpy(inp.A).to(dev), B=torch.from_numpy(inp.B).to(dev),
+            X=act(inp.X), dY=act(inp.dY),
+            Y=torch.empty((T, m), dtype=spec.torch_dtype, device=dev),
+            dX=torch.empty((T, k), dtype=spec.torch_dtype, device=dev),
+            dA=torch.empty((m, r), dtype=torch.float32, device=dev),
+            dB=torch.empty((r, k), dtype=torch.float32, device=dev)))
+        if li:
+            inp.X = inp.dY = None
+    # one forward and one backward workspace, sized for the largest layer, shared by all layers
+    # (the calls run one after another on one stream)
+    ws_f = lrqat.workspace(max(lrqat.lrqat_forward_workspace_size(l["spec"], T) for l in layers), dev)
+    ws_b = lrqat.workspace(max(lrqat.lrqat_backward_workspace_size(l["spec"], T) for l in layers), dev)
     stream = torch.cuda.current_stream()
 
     def step():
-        lrqat.lrqat_forward(spec, X, phi0, s0, A, B, Y=Y, ws=ws_f, stream=stream)
-        lrqat.lrqat_backward(spec, X, phi0, s0, A, B, dY, dX=dX, dA=dA, dB=dB, ws=ws_b, stream=stream)
+        for l in layers:
+            lrqat.lrqat_forward(l["spec"], l["X"], l["phi0"], l["s0"], l["A"], l["B"], Y=l["Y"], ws=ws_f,
+                                stream=stream)
+            lrqat.lrqat_backward(l["spec"], l["X"], l["phi0"], l["s0"], l["A"], l["B"], l["dY"], dX=l["dX"],
+                                 dA=l["dA"], dB=l["dB"], ws=ws_b, stream=stream)
 
     torch.cuda.synchronize()
     torch.cuda.reset_peak_memory_stats(dev)
@@ -249,31 +269,48 @@ def main():
     per = lrqat.lrqat_timing_read()
     lrqat.lrqat_timing_enable(False)
     lrqat.lrqat_timing_reset()
-    kernels = {n: {"launches": c, "avg_us": 1e3 * t / c} for n, (c, t) in per.items()}
+    nl = len(layers)
+    kernels = {n: {"launches": c, "avg_us": 1e3 * t / c, "us_per_step": 1e3 * t / args.steps}
+               for n, (c, t) in per.items()}
     dom = max(per, key=lambda n: per[n][1])
-    dom_avg_s = per[dom][1] / per[dom][0] * 1e-3
-    dom_flops = kernel_flops(dom, wl, lspec)
-    traffic = traffic_record(dom)
-    roofline = {"kernel": dom, "bound": "mfma", "achieved": dom_flops / dom_avg_s / 1e12 if dom_flops else None,
-                "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                "frac": (dom_flops / dom_avg_s / 1e12) / PEAK_BF16_TFLOPS if dom_flops else None,
-                "traffic": traffic}
+    dom_step_s = per[dom][1] / args.steps * 1e-3        # the dominant kernel's time per step
+    dom_flops = kernel_flops(dom, wl)                    # its algorithmic flops per step
+    traffic = traffic_record(dom) if nl == 1 else None
+    achieved = dom_flops / dom_step_s / 1e12 if dom_flops else None
+    roofline = {"kernel": dom, "bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                "frac": achieved / PEAK_BF16_TFLOPS if achieved else None, "traffic": traffic,
+                "avg_launch_us": 1e3 * per[dom][1] / per[dom][0], "launches_per_step": per[dom][0] // args.steps}
 
-    # merge (W_Z for inference) and a plain device copy, as bandwidth
-    merge_bytes = phi0.numel() * phi0.element_size() + 4 * (m + k) * r + m * k // 2
-    W_int4 = torch.empty((m, k // 2), dtype=torch.uint8, device=dev)
-    for _ in range(3):
-        lrqat.lrqat_merge_to_int4(spec, phi0, A, B, out=W_int4, stream=stream)
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record(stream)
-    for _ in range(20):
-        lrqat.lrqat_merge_to_int4(spec, phi0, A, B, out=W_int4, stream=stream)
-    e1.record(stream)
-    torch.cuda.synchronize()
-    merge_us = 1e3 * e0.elapsed_time(e1) / 20
+    # merge of every layer (W_Z for inference) and a plain device copy, as bandwidth
+    merge_bytes = sum(l["phi0"].numel() * l["phi0"].element_size() + 4 * (l["spec"].out_features +
+                      l["spec"].in_features) * r + l["spec"].out_features * l["spec"].in_features // 2
+                      for l in layers)
+    W_int4 = [torch.empty((l["spec"].out_features, l["spec"].in_features // 2), dtype=torch.uint8, device=dev)
+              for l in layers]
+
+    def merge_all():
+        for l, w in zip(layers, W_int4):
+            lrqat.lrqat_merge_to_int4(l["spec"], l["phi0"], l["A"], l["B"], out=w, stream=stream)
+
+    merge = None
+    if wl.bits <= 4:
+        for _ in range(3):
+            merge_all()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(20):
+            merge_all()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        merge_us = 1e3 * e0.elapsed_time(e1) / 20
+        merge = {"us": merge_us, "layers": nl, "algorithmic_bytes": merge_bytes,
+                 "GB/s": merge_bytes / (merge_us * 1e-6) / 1e9,
+                 "frac_of_hbm_peak": merge_bytes / (merge_us * 1e-6) / 1e9 / PEAK_HBM_GBS}
+    del W_int4
     src = torch.empty(256 << 18, dtype=torch.float32, device=dev)
     dst = torch.empty_like(src)
     dst.copy_(src)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record(stream)
     for _ in range(10):
         dst.copy_(src)
@@ -281,14 +318,18 @@ def main():
     torch.cuda.synchronize()
     copy_gbs = 2 * src.numel() * 4 * 10 / (e0.elapsed_time(e1) * 1e-3) / 1e9
     del src, dst
-    merge = {"us": merge_us, "algorithmic_bytes": merge_bytes, "GB/s": merge_bytes / (merge_us * 1e-6) / 1e9,
-             "frac_of_hbm_peak": merge_bytes / (merge_us * 1e-6) / 1e9 / PEAK_HBM_GBS,
-             "device_copy_GB/s": copy_gbs}
-    # device memory the layer holds across forward + backward (checkpointing: nothing saved but the inputs)
+    if merge:
+        merge["device_copy_GB/s"] = copy_gbs
+    # device memory the layers hold across forward + backward (checkpointing: nothing saved but the inputs)
     act_b = 2 if wl.act_dtype == "bf16" else 4
-    analytic = {"phi0": phi0.numel() * phi0.element_size(), "s": s0.numel() * 4, "A+B": 4 * (m + k) * r,
-                "X+dY": act_b * T * (k + m), "Y+dX": act_b * T * (m + k), "dA+dB": 4 * (m + k) * r,
+    analytic = {"phi0": sum(l["phi0"].numel() * l["phi0"].element_size() for l in layers),
+                "s": sum(l["s0"].numel() * 4 for l in layers),
+                "A+B": sum(4 * (L.m + L.k) * r for L in wl.layers),
+                "X+dY": sum(act_b * T * (L.k + L.m) for L in wl.layers),
+                "Y+dX": sum(act_b * T * (L.m + L.k) for L in wl.layers),
+                "dA+dB": sum(4 * (L.m + L.k) * r for L in wl.layers),
                 "workspace_fwd": ws_f.numel(), "workspace_bwd": ws_b.numel()}
+    inp = inp0
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -299,7 +340,8 @@ def main():
         "metric": METRIC, "value": value, "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "bf16" if wl.act_dtype == "bf16" else "fp32", "data": "synthetic",
-        "config": {"workload": wl.name, "tokens": T, "out_features": m, "in_features": k, "rank": r,
+        "config": {"workload": wl.name, "tokens": T,
+                   "layers": [[L.name, L.m, L.k] for L in wl.layers], "rank": r,
                    "alpha": wl.alpha, "bits": wl.bits, "phi_format": wl.phi_format, "group_size": wl.group_size,
                    "act_bits": wl.act_bits, "parallelism": "none"},
         "step_ms_p10_p50_p90": [float(np.percentile(per_step, q)) for q in (10, 50, 90)],

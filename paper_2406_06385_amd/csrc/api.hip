@@ -85,7 +85,7 @@ struct Workspace {
 lrqat_status check_layer(const lrqat_layer* L, Dims& d) {
   if (!L) return fail(LRQAT_EINVAL, "layer is NULL");
   if (L->out_features < 1 || L->in_features < 1 || L->out_features > kMaxDim || L->in_features > kMaxDim)
-    return fail(LRQAT_EINVAL, "out_features and in_features must be in [1, 2^30] (got %lld, %lld)",
+    return fail(LRQAT_EINVAL, "out_features and in_features must be in [1, 2^22] (got %lld, %lld)",
                 (long long)L->out_features, (long long)L->in_features);
   if (L->rank < 1 || L->rank > 256) return fail(LRQAT_EINVAL, "rank must be in [1, 256] (got %d)", L->rank);
   if (!std::isfinite(L->alpha)) return fail(LRQAT_EINVAL, "alpha must be finite");

@@ -126,9 +126,29 @@ def _stream(stream):
     return ctypes.c_void_p(s.cuda_stream)
 
 
-def _expect(t, shape, dtype, name):
+def _torch_stream(stream):
+    return torch.cuda.current_stream() if stream is None else stream
+
+
+def _expect(t, shape, dtype, name, device=None):
+    """Reject a tensor whose shape, dtype, layout or device the C ABI would
+    misread (the library sees only a pointer)."""
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name}: expected a torch.Tensor, got {type(t).__name__}")
     if tuple(t.shape) != tuple(shape) or t.dtype != dtype:
         raise ValueError(f"{name}: expected {tuple(shape)} {dtype}, got {tuple(t.shape)} {t.dtype}")
+    if not t.is_cuda or not t.is_contiguous():
+        raise ValueError(f"{name}: must be a contiguous GPU tensor")
+    if device is not None and t.device != device:
+        raise ValueError(f"{name}: on {t.device}, expected {device}")
+
+
+def _weights(spec: "LayerSpec", phi0, s, A, B, device):
+    m, k, r = spec.out_features, spec.in_features, spec.rank
+    _expect(phi0, spec.phi_shape(), spec.phi_dtype, "phi0", device)
+    _expect(s, spec.scale_shape(), torch.float32, "s", device)
+    _expect(A, (m, r), torch.float32, "A", device)
+    _expect(B, (r, k), torch.float32, "B", device)
 
 
 def lrqat_forward_workspace_size(spec: LayerSpec, tokens: int) -> int:
@@ -154,53 +174,80 @@ def workspace(nbytes: int, device="cuda") -> torch.Tensor:
 def lrqat_init_from_weights(spec: LayerSpec, W0: torch.Tensor, stream=None):
     """-> (s0 float32, Phi0) computed on the GPU from W0 [m][k] float32."""
     _expect(W0, (spec.out_features, spec.in_features), torch.float32, "W0")
-    s0 = torch.empty(spec.scale_shape(), dtype=torch.float32, device=W0.device)
-    phi0 = torch.empty(spec.phi_shape(), dtype=spec.phi_dtype, device=W0.device)
+    st = _torch_stream(stream)
+    with torch.cuda.stream(st):
+        s0 = torch.empty(spec.scale_shape(), dtype=torch.float32, device=W0.device)
+        phi0 = torch.empty(spec.phi_shape(), dtype=spec.phi_dtype, device=W0.device)
     L = spec.c_struct()
-    _check(_lib().lrqat_init_from_weights(ctypes.byref(L), _ptr(W0), _ptr(s0), _ptr(phi0), _stream(stream)))
+    _check(_lib().lrqat_init_from_weights(ctypes.byref(L), _ptr(W0), _ptr(s0), _ptr(phi0), _stream(st)))
     return s0, phi0
 
 
 def lrqat_forward(spec: LayerSpec, X, phi0, s, A, B, Y=None, ws=None, stream=None):
     """Y = X_hat W_hat^T.  X [T][k] in the layer's activation dtype."""
-    T = X.shape[0]
+    T = X.shape[0] if X.dim() == 2 else -1
     _expect(X, (T, spec.in_features), spec.torch_dtype, "X")
-    if Y is None:
-        Y = torch.empty((T, spec.out_features), dtype=spec.torch_dtype, device=X.device)
-    if ws is None:
-        ws = workspace(lrqat_forward_workspace_size(spec, T), X.device)
+    dev = X.device
+    _weights(spec, phi0, s, A, B, dev)
+    st = _torch_stream(stream)
+    with torch.cuda.stream(st):  # buffers made here belong to the stream the kernels run on
+        if Y is None:
+            Y = torch.empty((T, spec.out_features), dtype=spec.torch_dtype, device=dev)
+        if ws is None:
+            ws = workspace(lrqat_forward_workspace_size(spec, T), dev)
+    _expect(Y, (T, spec.out_features), spec.torch_dtype, "Y", dev)
+    _expect(ws, (ws.numel(),), torch.uint8, "ws", dev)
     L = spec.c_struct()
     _check(_lib().lrqat_forward(ctypes.byref(L), T, _ptr(X), _ptr(phi0), _ptr(s), _ptr(A), _ptr(B), _ptr(Y),
-                                _ptr(ws), ws.numel(), _stream(stream)))
+                                _ptr(ws), ws.numel(), _stream(st)))
     return Y
 
 
 def lrqat_backward(spec: LayerSpec, X, phi0, s, A, B, dY, dX=None, dA=None, dB=None, want_dx=True,
                    accumulate=False, ws=None, stream=None):
     """-> (dX or None, dA, dB) with the straight-through estimator; W_hat is recomputed."""
-    T = X.shape[0]
+    T = X.shape[0] if X.dim() == 2 else -1
     m, k, r = spec.out_features, spec.in_features, spec.rank
-    if dX is None and want_dx:
-        dX = torch.empty((T, k), dtype=spec.torch_dtype, device=X.device)
-    if dA is None:
-        dA = torch.empty((m, r), dtype=torch.float32, device=X.device)
-    if dB is None:
-        dB = torch.empty((r, k), dtype=torch.float32, device=X.device)
-    if ws is None:
-        ws = workspace(lrqat_backward_workspace_size(spec, T), X.device)
+    _expect(X, (T, k), spec.torch_dtype, "X")
+    dev = X.device
+    _weights(spec, phi0, s, A, B, dev)
+    _expect(dY, (T, m), spec.torch_dtype, "dY", dev)
+    st = _torch_stream(stream)
+    with torch.cuda.stream(st):
+        if dX is None and want_dx:
+            dX = torch.empty((T, k), dtype=spec.torch_dtype, device=dev)
+        if dA is None:
+            dA = torch.empty((m, r), dtype=torch.float32, device=dev)
+        if dB is None:
+            dB = torch.empty((r, k), dtype=torch.float32, device=dev)
+        if ws is None:
+            ws = workspace(lrqat_backward_workspace_size(spec, T), dev)
+    if dX is not None:
+        _expect(dX, (T, k), spec.torch_dtype, "dX", dev)
+    _expect(dA, (m, r), torch.float32, "dA", dev)
+    _expect(dB, (r, k), torch.float32, "dB", dev)
+    _expect(ws, (ws.numel(),), torch.uint8, "ws", dev)
     L = spec.c_struct()
     _check(_lib().lrqat_backward(ctypes.byref(L), T, _ptr(X), _ptr(phi0), _ptr(s), _ptr(A), _ptr(B), _ptr(dY),
                                  _ptr(dX), _ptr(dA), _ptr(dB), None, int(bool(accumulate)), _ptr(ws), ws.numel(),
-                                 _stream(stream)))
+                                 _stream(st)))
     return dX, dA, dB
 
 
 def lrqat_merge_to_int4(spec: LayerSpec, phi0, A, B, out=None, stream=None):
     """W_Z = clip(round(Phi0 + (alpha/r) A B)) double-packed, uint8 [m][k/2]."""
+    m, k, r = spec.out_features, spec.in_features, spec.rank
+    dev = A.device
+    _expect(phi0, spec.phi_shape(), spec.phi_dtype, "phi0", dev)
+    _expect(A, (m, r), torch.float32, "A", dev)
+    _expect(B, (r, k), torch.float32, "B", dev)
+    st = _torch_stream(stream)
     if out is None:
-        out = torch.empty((spec.out_features, spec.in_features // 2), dtype=torch.uint8, device=A.device)
+        with torch.cuda.stream(st):
+            out = torch.empty((m, k // 2), dtype=torch.uint8, device=dev)
+    _expect(out, (m, k // 2), torch.uint8, "out", dev)
     L = spec.c_struct()
-    _check(_lib().lrqat_merge_to_int4(ctypes.byref(L), _ptr(phi0), _ptr(A), _ptr(B), _ptr(out), _stream(stream)))
+    _check(_lib().lrqat_merge_to_int4(ctypes.byref(L), _ptr(phi0), _ptr(A), _ptr(B), _ptr(out), _stream(st)))
     return out
 
 

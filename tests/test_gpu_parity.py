@@ -8,7 +8,11 @@ element by element (small shapes) or on sampled rows/columns (full sizes).
 Criteria: integer grid and Phi0/s0/merge bytes bit-exact (a grid element may
 differ only when its pre-round value lies within 1e-5 of a .5 boundary, and
 such elements must stay below a 1e-4 fraction); Y, dX, dA, dB within a
-relative Frobenius error of 1e-4 (float32 activations) or 2e-2 (bfloat16).
+relative error of 1e-4 (float32 activations) or 2e-2 (bfloat16), measured
+three ways on every compared tensor: the Frobenius norm of the whole tensor,
+and the norm of every row and of every column against the norm of the same
+row or column of the reference (a row or column that is zero in the
+reference must be zero on the device, up to 1e-6 of the tensor's RMS).
 """
 import math
 import sys
@@ -44,6 +48,50 @@ def rel_fro(dev, ref):
     dev = np.asarray(dev, np.float64)
     ref = np.asarray(ref, np.float64)
     return float(np.linalg.norm(dev - ref) / max(np.linalg.norm(ref), 1e-300))
+
+
+def line_errors(dev, ref, axis, den=None):
+    """Relative errors of the rows (axis=1) or columns (axis=0):
+    ||dev_line - ref_line|| / ||den_line|| (den = ref by default).  Lines
+    that are zero in the denominator count as exact when the device's line
+    is below 1e-6 of the reference's RMS, else as an error of 1."""
+    dev = np.asarray(dev, np.float64)
+    ref = np.asarray(ref, np.float64)
+    den = ref if den is None else np.asarray(den, np.float64)
+    if dev.ndim == 1:
+        dev, ref, den = dev[:, None], ref[:, None], den[:, None]
+    num = np.linalg.norm(dev - ref, axis=axis)
+    dnorm = np.linalg.norm(den, axis=axis)
+    rms = np.sqrt(np.mean(ref * ref)) if ref.size else 0.0
+    zero = dnorm == 0
+    out = np.where(zero, 0.0, num / np.where(zero, 1.0, dnorm))
+    bad_zero = zero & (np.linalg.norm(dev, axis=axis) > 1e-6 * rms * np.sqrt(ref.shape[axis]))
+    out[bad_zero] = 1.0
+    return out
+
+
+def errors(dev, ref, mag=None, tol=None):
+    """(Frobenius, worst row, worst column) relative errors of one tensor.
+
+    With `mag` (the magnitudes of the terms summed into each element, for the
+    rank-r gradient contractions), a row or column whose own error ratio
+    exceeds the tolerance still counts as within it when its error is below
+    2^-6 of the norm of the same line of `mag` (reported scaled by tol/2^-6):
+    the contraction runs on bfloat16 operands (the gradient G in the compute
+    data type), each rounded to 2^-9 relative, so cancellation inside a sum
+    limits the accuracy relative to the terms, not to the result."""
+    out = [rel_fro(dev, ref)]
+    for axis in (1, 0):
+        e = line_errors(dev, ref, axis)
+        if mag is not None:
+            e = np.minimum(e, line_errors(dev, ref, axis, den=mag) * (tol / 2.0 ** -6))
+        out.append(float(e.max()) if e.size else 0.0)
+    return tuple(out)
+
+
+def assert_close(errs, tol):
+    for name, e in errs.items():
+        assert max(e) < tol, (name, e, tol)
 
 
 def to_dev_act(a, dtype):
@@ -151,10 +199,14 @@ def check_full(lr, c, accumulate=False):
         gr["dA"] = gr["dA"] + 0.25
         gr["dB"] = gr["dB"] - 0.5
     tol = TOL[c.dtype]
-    errs = {"Y": rel_fro(Y, Yr), "dX": rel_fro(dX, gr["dX"]), "dA": rel_fro(dA, gr["dA"]), "dB": rel_fro(dB, gr["dB"])}
-    _log(f"  errors {errs}")
-    for k_, e in errs.items():
-        assert e < tol, (k_, e, tol)
+    allr, allc = np.arange(L.m), np.arange(L.k)
+    mA = O.da_rows_abs(L, c.Xv, c.phi0_ref, c.s0_ref, c.A, c.B, c.dYv, allr)
+    mB = O.db_cols_abs(L, c.Xv, c.phi0_ref, c.s0_ref, c.A, c.B, c.dYv, allc)
+    errs = {"Y": errors(Y, Yr), "dX": errors(dX, gr["dX"]),
+            "dA": errors(dA, gr["dA"], None if accumulate else mA, tol),
+            "dB": errors(dB, gr["dB"], None if accumulate else mB, tol)}
+    _log(f"  errors (fro, row, col) {errs}")
+    assert_close(errs, tol)
     return errs
 
 
@@ -168,14 +220,15 @@ def check_sampled(lr, c, n_tok=48, n_rows=24, n_cols=24, seed=0):
     cols = np.unique(np.concatenate([[0, L.k - 1], rng.integers(0, L.k, n_cols)]))
     tol = TOL[c.dtype]
     errs = {
-        "Y": rel_fro(Y[tok], O.forward_rows(L, c.Xv, c.phi0_ref, c.s0_ref, c.A, c.B, tok)),
-        "dX": rel_fro(dX[tok], O.dx_rows(L, c.phi0_ref, c.s0_ref, c.A, c.B, c.dYv, tok)),
-        "dA": rel_fro(dA[rows], O.da_rows(L, c.Xv, c.phi0_ref, c.s0_ref, c.A, c.B, c.dYv, rows)),
-        "dB": rel_fro(dB[:, cols], O.db_cols(L, c.Xv, c.phi0_ref, c.s0_ref, c.A, c.B, c.dYv, cols)),
+        "Y": errors(Y[tok], O.forward_rows(L, c.Xv, c.phi0_ref, c.s0_ref, c.A, c.B, tok)),
+        "dX": errors(dX[tok], O.dx_rows(L, c.phi0_ref, c.s0_ref, c.A, c.B, c.dYv, tok)),
+        "dA": errors(dA[rows], O.da_rows(L, c.Xv, c.phi0_ref, c.s0_ref, c.A, c.B, c.dYv, rows),
+                     O.da_rows_abs(L, c.Xv, c.phi0_ref, c.s0_ref, c.A, c.B, c.dYv, rows), tol),
+        "dB": errors(dB[:, cols], O.db_cols(L, c.Xv, c.phi0_ref, c.s0_ref, c.A, c.B, c.dYv, cols),
+                     O.db_cols_abs(L, c.Xv, c.phi0_ref, c.s0_ref, c.A, c.B, c.dYv, cols), tol),
     }
-    _log(f"  sampled errors {errs}")
-    for k_, e in errs.items():
-        assert e < tol, (k_, e, tol)
+    _log(f"  sampled errors (fro, row, col) {errs}")
+    assert_close(errs, tol)
     assert np.isfinite(Y).all() and np.isfinite(dX).all() and np.isfinite(dA).all() and np.isfinite(dB).all()
 
 
@@ -194,7 +247,8 @@ def test_workload_full_or_sampled(lr, cfg):
         check_sampled(lr, c)
 
 
-@pytest.mark.parametrize("cfg,layer", [(3, 0), (3, 2), (4, 0), (4, 1), (5, 1), (5, 6)])
+@pytest.mark.parametrize("cfg,layer", [(3, 0), (3, 1), (3, 2), (4, 0), (4, 1),
+                                       (5, 0), (5, 1), (5, 2), (5, 3), (5, 4), (5, 5), (5, 6)])
 def test_workload_sampled_full_size(lr, cfg, layer):
     wl = I.WORKLOADS[cfg]
     _log(f"[workload {cfg} layer {wl.layers[layer].name}] m={wl.layers[layer].m} k={wl.layers[layer].k}")
