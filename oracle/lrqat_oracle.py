@@ -470,11 +470,26 @@ def loftq_init(W0: np.ndarray, s0: np.ndarray, bits: int, group_size: int, rank:
 
 
 # ----------------------------------------------------------------------------- error scales
-# Magnitudes of the terms of the rank-r gradient contractions, c |G| |B|^T and
-# c |A|^T |G| (|.| elementwise).  A contraction whose operands carry a relative
-# rounding error e is accurate to about e times these, whatever the
-# cancellation inside the sums; the parity tests use them as the scale of the
-# bound for dA and dB lines whose own norm is small against them.
+# Magnitudes of the terms of the layer's contractions: |X_hat| |W_hat|^T for Y,
+# |dY| |W_hat| for dX, c |G| |B|^T for dA and c |A|^T |G| for dB (|.|
+# elementwise).  A contraction whose operands carry a relative rounding error e
+# is accurate to about e times these, whatever the cancellation inside the
+# sums; the parity tests use them as the scale of the bound for output lines
+# whose own norm is small against them.
+
+def forward_rows_abs(L: Layer, X, phi0, s, A, B, tok, z=None):
+    """Rows `tok` of |X_hat| |W_hat|^T."""
+    q, _, _, _ = grid_from_inputs(phi0, A, B, L.alpha, L.rank, L.bits, L.fmt)
+    W = np.abs(weight_hat(q, s, L.group_size, z))
+    return np.abs(layer_input(np.asarray(X)[tok], L.act_bits)) @ W.T
+
+
+def dx_rows_abs(L: Layer, phi0, s, A, B, dY, tok, z=None):
+    """Rows `tok` of |dY| |W_hat|."""
+    q, _, _, _ = grid_from_inputs(phi0, A, B, L.alpha, L.rank, L.bits, L.fmt)
+    W = np.abs(weight_hat(q, s, L.group_size, z))
+    return np.abs(np.asarray(dY, np.float64)[tok]) @ W
+
 
 def _abs_g(L: Layer, X, phi0, s, A, B, dY, rows=None, cols=None):
     q, M, _, _ = grid_from_inputs(phi0, A, B, L.alpha, L.rank, L.bits, L.fmt)

@@ -73,13 +73,14 @@ def line_errors(dev, ref, axis, den=None):
 def errors(dev, ref, mag=None, tol=None):
     """(Frobenius, worst row, worst column) relative errors of one tensor.
 
-    With `mag` (the magnitudes of the terms summed into each element, for the
-    rank-r gradient contractions), a row or column whose own error ratio
-    exceeds the tolerance still counts as within it when its error is below
-    2^-6 of the norm of the same line of `mag` (reported scaled by tol/2^-6):
-    the contraction runs on bfloat16 operands (the gradient G in the compute
-    data type), each rounded to 2^-9 relative, so cancellation inside a sum
-    limits the accuracy relative to the terms, not to the result."""
+    With `mag` (the magnitudes of the terms summed into each element), a row
+    or column whose own error ratio exceeds the tolerance still counts as
+    within it when its error is below 2^-6 of the norm of the same line of
+    `mag` (reported scaled by tol/2^-6): the contractions run on bfloat16
+    operands (the weight tile s q where s is folded in, the gradient G in the
+    compute data type), each rounded to 2^-9 relative, so cancellation inside a
+    sum limits the accuracy relative to the terms, not to the result (a line
+    of one element, as a column of Y at T = 1, is a single such sum)."""
     out = [rel_fro(dev, ref)]
     for axis in (1, 0):
         e = line_errors(dev, ref, axis)
@@ -202,7 +203,10 @@ def check_full(lr, c, accumulate=False):
     allr, allc = np.arange(L.m), np.arange(L.k)
     mA = O.da_rows_abs(L, c.Xv, c.phi0_ref, c.s0_ref, c.A, c.B, c.dYv, allr)
     mB = O.db_cols_abs(L, c.Xv, c.phi0_ref, c.s0_ref, c.A, c.B, c.dYv, allc)
-    errs = {"Y": errors(Y, Yr), "dX": errors(dX, gr["dX"]),
+    allt = np.arange(c.T)
+    mY = O.forward_rows_abs(L, c.Xv, c.phi0_ref, c.s0_ref, c.A, c.B, allt)
+    mX = O.dx_rows_abs(L, c.phi0_ref, c.s0_ref, c.A, c.B, c.dYv, allt)
+    errs = {"Y": errors(Y, Yr, mY, tol), "dX": errors(dX, gr["dX"], mX, tol),
             "dA": errors(dA, gr["dA"], None if accumulate else mA, tol),
             "dB": errors(dB, gr["dB"], None if accumulate else mB, tol)}
     _log(f"  errors (fro, row, col) {errs}")
@@ -220,8 +224,10 @@ def check_sampled(lr, c, n_tok=48, n_rows=24, n_cols=24, seed=0):
     cols = np.unique(np.concatenate([[0, L.k - 1], rng.integers(0, L.k, n_cols)]))
     tol = TOL[c.dtype]
     errs = {
-        "Y": errors(Y[tok], O.forward_rows(L, c.Xv, c.phi0_ref, c.s0_ref, c.A, c.B, tok)),
-        "dX": errors(dX[tok], O.dx_rows(L, c.phi0_ref, c.s0_ref, c.A, c.B, c.dYv, tok)),
+        "Y": errors(Y[tok], O.forward_rows(L, c.Xv, c.phi0_ref, c.s0_ref, c.A, c.B, tok),
+                    O.forward_rows_abs(L, c.Xv, c.phi0_ref, c.s0_ref, c.A, c.B, tok), tol),
+        "dX": errors(dX[tok], O.dx_rows(L, c.phi0_ref, c.s0_ref, c.A, c.B, c.dYv, tok),
+                     O.dx_rows_abs(L, c.phi0_ref, c.s0_ref, c.A, c.B, c.dYv, tok), tol),
         "dA": errors(dA[rows], O.da_rows(L, c.Xv, c.phi0_ref, c.s0_ref, c.A, c.B, c.dYv, rows),
                      O.da_rows_abs(L, c.Xv, c.phi0_ref, c.s0_ref, c.A, c.B, c.dYv, rows), tol),
         "dB": errors(dB[:, cols], O.db_cols(L, c.Xv, c.phi0_ref, c.s0_ref, c.A, c.B, c.dYv, cols),
