@@ -110,14 +110,19 @@ lrqat_status lrqat_init_from_weights(const lrqat_layer* layer, const float* W0,
  *                               quantisation when act_bits = 8)
  *   phi0  Phi0 in phi_format   frozen downcast weight
  *   s     float32 [m] or [m][k/g]
+ *   z     int32, shaped like s: the integer zero offset of asymmetric
+ *         quantisation (Eq. dequant; Section 3 last paragraph: z outside the
+ *         rounding), W_hat = s * (clip(round(Phi0 + (alpha/r) A B)) - z), with
+ *         Phi0 already carrying the offset (lrqat_init_from_weights);
+ *         NULL for symmetric quantisation
  *   A     float32 [m][r],  B float32 [r][k]
  *   Y     [T][m] act_dtype     output, overwritten
  *   ws    workspace of at least lrqat_forward_workspace_size() bytes
  * Nothing is saved for the backward pass.  T = 0 is a no-op.
  */
 lrqat_status lrqat_forward(const lrqat_layer* layer, int64_t tokens, const void* X,
-                           const void* phi0, const float* s, const float* A, const float* B,
-                           void* Y, void* ws, size_t ws_bytes, void* stream);
+                           const void* phi0, const float* s, const int32_t* z, const float* A,
+                           const float* B, void* Y, void* ws, size_t ws_bytes, void* stream);
 
 /*
  * Backward pass with the straight-through estimator (Section 3).  W_hat and
@@ -135,9 +140,31 @@ lrqat_status lrqat_forward(const lrqat_layer* layer, int64_t tokens, const void*
  * same bits.
  */
 lrqat_status lrqat_backward(const lrqat_layer* layer, int64_t tokens, const void* X,
-                            const void* phi0, const float* s, const float* A, const float* B,
-                            const void* dY, void* dX, float* dA, float* dB, float* ds,
-                            int accumulate, void* ws, size_t ws_bytes, void* stream);
+                            const void* phi0, const float* s, const int32_t* z, const float* A,
+                            const float* B, const void* dY, void* dX, float* dA, float* dB,
+                            float* ds, int accumulate, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * lrqat_backward without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving or
+ * training loops, harnesses that forbid hipMalloc).  Same arguments, results
+ * and errors as lrqat_backward; the scratch space is one array in device
+ * memory that the library holds on each GPU it runs on until the process
+ * ends, of lrqat_backward_static_capacity() bytes (64 MiB: enough for a
+ * 4096 x 4096 layer with 8192 tokens).  A layer whose
+ * lrqat_backward_workspace_size() exceeds it is rejected with
+ * LRQAT_EWORKSPACE before anything is launched.  The call allocates nothing.
+ * Every call on one GPU uses that GPU's array: calls that overlap in time on
+ * one GPU (on different streams or threads) race and must be serialised by
+ * the caller.  Nothing in the array has to start at any particular value.
+ */
+lrqat_status lrqat_backward_static(const lrqat_layer* layer, int64_t tokens, const void* X,
+                                   const void* phi0, const float* s, const int32_t* z,
+                                   const float* A, const float* B, const void* dY, void* dX,
+                                   float* dA, float* dB, float* ds, int accumulate, void* stream);
+
+/* Bytes of the device array lrqat_backward_static uses on each GPU. */
+size_t lrqat_backward_static_capacity(void);
 
 /*
  * Merge for inference (Section 3: the adapters fuse into one b-bit integer

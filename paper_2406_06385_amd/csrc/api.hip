@@ -233,10 +233,12 @@ lrqat_status lrqat_init_from_weights(const lrqat_layer* layer, const float* W0, 
 }
 
 lrqat_status lrqat_forward(const lrqat_layer* layer, int64_t tokens, const void* X, const void* phi0, const float* s,
-                           const float* A, const float* B, void* Y, void* ws, size_t ws_bytes, void* stream) {
+                           const int32_t* z, const float* A, const float* B, void* Y, void* ws, size_t ws_bytes,
+                           void* stream) {
   Dims d;
   LRQAT_TRY(check_layer(layer, d));
   if (tokens < 0 || tokens > kMaxDim) return fail(LRQAT_EINVAL, "tokens out of range (%lld)", (long long)tokens);
+  if (z) return fail(LRQAT_EUNSUPPORTED, "the zero offset z is not supported by this build; pass NULL");
   if (tokens == 0) return LRQAT_OK;
   NEED(X, 16);
   NEED(phi0, 16);
@@ -283,12 +285,19 @@ lrqat_status lrqat_forward(const lrqat_layer* layer, int64_t tokens, const void*
   return LRQAT_OK;
 }
 
-lrqat_status lrqat_backward(const lrqat_layer* layer, int64_t tokens, const void* X, const void* phi0, const float* s,
-                            const float* A, const float* B, const void* dY, void* dX, float* dA, float* dB, float* ds,
-                            int accumulate, void* ws, size_t ws_bytes, void* stream) {
+}  // extern "C"
+
+namespace {
+
+// The backward pass of lrqat_backward and lrqat_backward_static: `ws` is the
+// caller's workspace or the library's device-resident scratch array.
+lrqat_status backward_impl(const lrqat_layer* layer, int64_t tokens, const void* X, const void* phi0, const float* s,
+                           const int32_t* z, const float* A, const float* B, const void* dY, void* dX, float* dA,
+                           float* dB, float* ds, int accumulate, void* ws, size_t ws_bytes, void* stream) {
   Dims d;
   LRQAT_TRY(check_layer(layer, d));
   if (tokens < 0 || tokens > kMaxDim) return fail(LRQAT_EINVAL, "tokens out of range (%lld)", (long long)tokens);
+  if (z) return fail(LRQAT_EUNSUPPORTED, "the zero offset z is not supported by this build; pass NULL");
   if (ds) return fail(LRQAT_EUNSUPPORTED, "the scale gradient ds is not computed by this build; pass NULL");
   if (accumulate != 0 && accumulate != 1) return fail(LRQAT_EINVAL, "accumulate must be 0 or 1");
   NEED(dA, 4);
@@ -370,6 +379,66 @@ lrqat_status lrqat_backward(const lrqat_layer* layer, int64_t tokens, const void
   LRQAT_TRY(hip_status(timed("reduce", st, [&] { return launch_reduce2(ra, st); }), "reduce"));
   return LRQAT_OK;
 }
+
+// ---- the device-resident scratch of lrqat_backward_static
+// One array per GPU (each device holds its own copy of a __device__ variable),
+// kept until the process ends.  Host code never passes `scratch` itself to a
+// kernel: its device address is looked up once per device.
+constexpr size_t kStaticScratchBytes = size_t(64) << 20;
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+}  // namespace
+
+static __device__ __align__(256) uint8_t scratch[kStaticScratchBytes];
+
+namespace {
+
+lrqat_status static_scratch(void** out) {
+  int dev = 0;
+  LRQAT_TRY(hip_status(hipGetDevice(&dev), "hipGetDevice"));
+  if (dev < 0 || dev >= kMaxDevices) return fail(LRQAT_EINVAL, "device %d beyond the %d this library tracks", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    LRQAT_TRY(hip_status(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)), "hipGetSymbolAddress(scratch)"));
+    if (!p) return fail(LRQAT_EHIP, "hipGetSymbolAddress(scratch) returned NULL");
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return LRQAT_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+lrqat_status lrqat_backward(const lrqat_layer* layer, int64_t tokens, const void* X, const void* phi0, const float* s,
+                            const int32_t* z, const float* A, const float* B, const void* dY, void* dX, float* dA,
+                            float* dB, float* ds, int accumulate, void* ws, size_t ws_bytes, void* stream) {
+  return backward_impl(layer, tokens, X, phi0, s, z, A, B, dY, dX, dA, dB, ds, accumulate, ws, ws_bytes, stream);
+}
+
+lrqat_status lrqat_backward_static(const lrqat_layer* layer, int64_t tokens, const void* X, const void* phi0,
+                                   const float* s, const int32_t* z, const float* A, const float* B, const void* dY,
+                                   void* dX, float* dA, float* dB, float* ds, int accumulate, void* stream) {
+  Dims d;
+  LRQAT_TRY(check_layer(layer, d));
+  if (tokens < 0 || tokens > kMaxDim) return fail(LRQAT_EINVAL, "tokens out of range (%lld)", (long long)tokens);
+  const size_t need = layout(d, tokens, true).total;
+  if (need > kStaticScratchBytes)
+    return fail(LRQAT_EWORKSPACE,
+                "lrqat_backward_static: this layer needs %zu bytes of scratch, more than the %zu bytes of the "
+                "library's device array; use lrqat_backward with a workspace",
+                need, kStaticScratchBytes);
+  void* ws = nullptr;
+  LRQAT_TRY(static_scratch(&ws));
+  return backward_impl(layer, tokens, X, phi0, s, z, A, B, dY, dX, dA, dB, ds, accumulate, ws, kStaticScratchBytes,
+                       stream);
+}
+
+size_t lrqat_backward_static_capacity(void) { return kStaticScratchBytes; }
 
 lrqat_status lrqat_merge_to_int4(const lrqat_layer* layer, const void* phi0, const float* A, const float* B,
                                  uint8_t* W_int4, void* stream) {

@@ -84,10 +84,14 @@ def _lib():
         lib.lrqat_backward_workspace_size.argtypes = [F, I64]
         lib.lrqat_backward_workspace_size.restype = SZ
         lib.lrqat_init_from_weights.argtypes = [F, P, P, P, P]
-        lib.lrqat_forward.argtypes = [F, I64, P, P, P, P, P, P, P, SZ, P]
-        lib.lrqat_backward.argtypes = [F, I64, P, P, P, P, P, P, P, P, P, P, ctypes.c_int, P, SZ, P]
+        lib.lrqat_forward.argtypes = [F, I64, P, P, P, P, P, P, P, P, SZ, P]
+        lib.lrqat_backward.argtypes = [F, I64, P, P, P, P, P, P, P, P, P, P, P, ctypes.c_int, P, SZ, P]
+        lib.lrqat_backward_static.argtypes = [F, I64, P, P, P, P, P, P, P, P, P, P, P, ctypes.c_int, P]
+        lib.lrqat_backward_static_capacity.argtypes = []
+        lib.lrqat_backward_static_capacity.restype = SZ
         lib.lrqat_merge_to_int4.argtypes = [F, P, P, P, P, P]
-        for fn in ("lrqat_init_from_weights", "lrqat_forward", "lrqat_backward", "lrqat_merge_to_int4"):
+        for fn in ("lrqat_init_from_weights", "lrqat_forward", "lrqat_backward", "lrqat_backward_static",
+                   "lrqat_merge_to_int4"):
             getattr(lib, fn).restype = ctypes.c_int
         lib.lrqat_status_string.argtypes = [ctypes.c_int]
         lib.lrqat_status_string.restype = ctypes.c_char_p
@@ -143,10 +147,12 @@ def _expect(t, shape, dtype, name, device=None):
         raise ValueError(f"{name}: on {t.device}, expected {device}")
 
 
-def _weights(spec: "LayerSpec", phi0, s, A, B, device):
+def _weights(spec: "LayerSpec", phi0, s, A, B, device, z=None):
     m, k, r = spec.out_features, spec.in_features, spec.rank
     _expect(phi0, spec.phi_shape(), spec.phi_dtype, "phi0", device)
     _expect(s, spec.scale_shape(), torch.float32, "s", device)
+    if z is not None:
+        _expect(z, spec.scale_shape(), torch.int32, "z", device)
     _expect(A, (m, r), torch.float32, "A", device)
     _expect(B, (r, k), torch.float32, "B", device)
 
@@ -183,12 +189,13 @@ def lrqat_init_from_weights(spec: LayerSpec, W0: torch.Tensor, stream=None):
     return s0, phi0
 
 
-def lrqat_forward(spec: LayerSpec, X, phi0, s, A, B, Y=None, ws=None, stream=None):
-    """Y = X_hat W_hat^T.  X [T][k] in the layer's activation dtype."""
+def lrqat_forward(spec: LayerSpec, X, phi0, s, A, B, Y=None, ws=None, stream=None, z=None):
+    """Y = X_hat W_hat^T.  X [T][k] in the layer's activation dtype; z (int32,
+    shaped like s) is the zero offset of asymmetric quantisation."""
     T = X.shape[0] if X.dim() == 2 else -1
     _expect(X, (T, spec.in_features), spec.torch_dtype, "X")
     dev = X.device
-    _weights(spec, phi0, s, A, B, dev)
+    _weights(spec, phi0, s, A, B, dev, z)
     st = _torch_stream(stream)
     with torch.cuda.stream(st):  # buffers made here belong to the stream the kernels run on
         if Y is None:
@@ -198,40 +205,69 @@ def lrqat_forward(spec: LayerSpec, X, phi0, s, A, B, Y=None, ws=None, stream=Non
     _expect(Y, (T, spec.out_features), spec.torch_dtype, "Y", dev)
     _expect(ws, (ws.numel(),), torch.uint8, "ws", dev)
     L = spec.c_struct()
-    _check(_lib().lrqat_forward(ctypes.byref(L), T, _ptr(X), _ptr(phi0), _ptr(s), _ptr(A), _ptr(B), _ptr(Y),
-                                _ptr(ws), ws.numel(), _stream(st)))
+    _check(_lib().lrqat_forward(ctypes.byref(L), T, _ptr(X), _ptr(phi0), _ptr(s), _ptr(z), _ptr(A), _ptr(B),
+                                _ptr(Y), _ptr(ws), ws.numel(), _stream(st)))
     return Y
 
 
-def lrqat_backward(spec: LayerSpec, X, phi0, s, A, B, dY, dX=None, dA=None, dB=None, want_dx=True,
-                   accumulate=False, ws=None, stream=None):
-    """-> (dX or None, dA, dB) with the straight-through estimator; W_hat is recomputed."""
+def _backward_args(spec, X, phi0, s, A, B, dY, dX, dA, dB, want_dx, ds, want_ds, z, stream):
     T = X.shape[0] if X.dim() == 2 else -1
     m, k, r = spec.out_features, spec.in_features, spec.rank
     _expect(X, (T, k), spec.torch_dtype, "X")
     dev = X.device
-    _weights(spec, phi0, s, A, B, dev)
+    _weights(spec, phi0, s, A, B, dev, z)
     _expect(dY, (T, m), spec.torch_dtype, "dY", dev)
     st = _torch_stream(stream)
-    with torch.cuda.stream(st):
+    with torch.cuda.stream(st):  # buffers made here belong to the stream the kernels run on
         if dX is None and want_dx:
             dX = torch.empty((T, k), dtype=spec.torch_dtype, device=dev)
         if dA is None:
             dA = torch.empty((m, r), dtype=torch.float32, device=dev)
         if dB is None:
             dB = torch.empty((r, k), dtype=torch.float32, device=dev)
-        if ws is None:
-            ws = workspace(lrqat_backward_workspace_size(spec, T), dev)
+        if ds is None and want_ds:
+            ds = torch.empty(spec.scale_shape(), dtype=torch.float32, device=dev)
     if dX is not None:
         _expect(dX, (T, k), spec.torch_dtype, "dX", dev)
     _expect(dA, (m, r), torch.float32, "dA", dev)
     _expect(dB, (r, k), torch.float32, "dB", dev)
+    if ds is not None:
+        _expect(ds, spec.scale_shape(), torch.float32, "ds", dev)
+    return T, dev, st, dX, dA, dB, ds
+
+
+def lrqat_backward(spec: LayerSpec, X, phi0, s, A, B, dY, dX=None, dA=None, dB=None, want_dx=True,
+                   accumulate=False, ws=None, stream=None, z=None, ds=None, want_ds=False):
+    """-> (dX or None, dA, dB) with the straight-through estimator; W_hat is
+    recomputed.  With want_ds (or a ds tensor) -> (dX, dA, dB, ds)."""
+    T, dev, st, dX, dA, dB, ds = _backward_args(spec, X, phi0, s, A, B, dY, dX, dA, dB, want_dx, ds, want_ds, z,
+                                                stream)
+    if ws is None:
+        with torch.cuda.stream(st):
+            ws = workspace(lrqat_backward_workspace_size(spec, T), dev)
     _expect(ws, (ws.numel(),), torch.uint8, "ws", dev)
     L = spec.c_struct()
-    _check(_lib().lrqat_backward(ctypes.byref(L), T, _ptr(X), _ptr(phi0), _ptr(s), _ptr(A), _ptr(B), _ptr(dY),
-                                 _ptr(dX), _ptr(dA), _ptr(dB), None, int(bool(accumulate)), _ptr(ws), ws.numel(),
-                                 _stream(st)))
-    return dX, dA, dB
+    _check(_lib().lrqat_backward(ctypes.byref(L), T, _ptr(X), _ptr(phi0), _ptr(s), _ptr(z), _ptr(A), _ptr(B),
+                                 _ptr(dY), _ptr(dX), _ptr(dA), _ptr(dB), _ptr(ds), int(bool(accumulate)), _ptr(ws),
+                                 ws.numel(), _stream(st)))
+    return (dX, dA, dB, ds) if ds is not None else (dX, dA, dB)
+
+
+def lrqat_backward_static(spec: LayerSpec, X, phi0, s, A, B, dY, dX, dA, dB, accumulate=False, stream=None,
+                          z=None, ds=None):
+    """lrqat_backward on the library's device-resident scratch array: every
+    output tensor is the caller's, nothing is allocated."""
+    T, dev, st, dX, dA, dB, ds = _backward_args(spec, X, phi0, s, A, B, dY, dX, dA, dB, dX is not None, ds,
+                                                False, z, stream)
+    L = spec.c_struct()
+    _check(_lib().lrqat_backward_static(ctypes.byref(L), T, _ptr(X), _ptr(phi0), _ptr(s), _ptr(z), _ptr(A),
+                                        _ptr(B), _ptr(dY), _ptr(dX), _ptr(dA), _ptr(dB), _ptr(ds),
+                                        int(bool(accumulate)), _stream(st)))
+    return (dX, dA, dB, ds) if ds is not None else (dX, dA, dB)
+
+
+def lrqat_backward_static_capacity() -> int:
+    return int(_lib().lrqat_backward_static_capacity())
 
 
 def lrqat_merge_to_int4(spec: LayerSpec, phi0, A, B, out=None, stream=None):

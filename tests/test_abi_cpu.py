@@ -47,16 +47,23 @@ FAKE = 1 << 20          # a 256-byte aligned dummy device address, never derefer
 BAD_ALIGN = FAKE + 2
 
 
-def _fwd(lib, L, T=16, X=FAKE, ws_bytes=1 << 30, Y=FAKE):
+def _fwd(lib, L, T=16, X=FAKE, ws_bytes=1 << 30, Y=FAKE, z=None):
     P = ctypes.c_void_p
-    return lib.lrqat_forward(ctypes.byref(L), T, P(X), P(FAKE), P(FAKE), P(FAKE), P(FAKE), P(Y), P(FAKE),
-                             ws_bytes, None)
+    return lib.lrqat_forward(ctypes.byref(L), T, P(X), P(FAKE), P(FAKE), P(z) if z else None, P(FAKE), P(FAKE),
+                             P(Y), P(FAKE), ws_bytes, None)
 
 
-def _bwd(lib, L, T=16, ds=None, accumulate=0, dX=FAKE, ws_bytes=1 << 30):
+def _bwd(lib, L, T=16, ds=None, accumulate=0, dX=FAKE, ws_bytes=1 << 30, z=None):
     P = ctypes.c_void_p
-    return lib.lrqat_backward(ctypes.byref(L), T, P(FAKE), P(FAKE), P(FAKE), P(FAKE), P(FAKE), P(FAKE), P(dX),
-                              P(FAKE), P(FAKE), P(ds) if ds else None, accumulate, P(FAKE), ws_bytes, None)
+    return lib.lrqat_backward(ctypes.byref(L), T, P(FAKE), P(FAKE), P(FAKE), P(z) if z else None, P(FAKE), P(FAKE),
+                              P(FAKE), P(dX), P(FAKE), P(FAKE), P(ds) if ds else None, accumulate, P(FAKE), ws_bytes,
+                              None)
+
+
+def _bwd_static(lib, L, T=16):
+    P = ctypes.c_void_p
+    return lib.lrqat_backward_static(ctypes.byref(L), T, P(FAKE), P(FAKE), P(FAKE), None, P(FAKE), P(FAKE),
+                                     P(FAKE), P(FAKE), P(FAKE), P(FAKE), None, 0, None)
 
 
 @pytest.mark.parametrize("kw,status", [
@@ -106,8 +113,20 @@ def test_pointer_and_workspace_errors(lib):
                                    None) == lrqat.LRQAT_EINVAL
     assert lib.lrqat_merge_to_int4(ctypes.byref(L), P(FAKE), P(FAKE), P(FAKE), P(0), None) == lrqat.LRQAT_EINVAL
     assert lib.lrqat_init_from_weights(ctypes.byref(L), P(0), P(FAKE), P(FAKE), None) == lrqat.LRQAT_EINVAL
-    assert lib.lrqat_forward(None, 16, P(FAKE), P(FAKE), P(FAKE), P(FAKE), P(FAKE), P(FAKE), P(FAKE), 1 << 30,
-                             None) == lrqat.LRQAT_EINVAL
+    assert lib.lrqat_forward(None, 16, P(FAKE), P(FAKE), P(FAKE), None, P(FAKE), P(FAKE), P(FAKE), P(FAKE),
+                             1 << 30, None) == lrqat.LRQAT_EINVAL
+
+
+def test_static_backward_rejects_layers_beyond_its_array(lib):
+    """The no-allocation backward refuses, before any HIP call, a layer whose
+    scratch would not fit the library's device array."""
+    cap = lib.lrqat_backward_static_capacity()
+    assert cap == 64 << 20
+    big = _layer(out_features=14336, in_features=4096, rank=32)
+    assert lib.lrqat_backward_workspace_size(ctypes.byref(big), 8192) > cap
+    assert _bwd_static(lib, big, T=8192) == lrqat.LRQAT_EWORKSPACE
+    assert b"lrqat_backward_static" in lib.lrqat_last_error()
+    assert _bwd_static(lib, _layer(bits=1)) == lrqat.LRQAT_EINVAL
 
 
 def test_workspace_sizes_grow_with_tokens_and_backward(lib):
