@@ -21,8 +21,10 @@
  *     caller; the library keeps no pointer after a call returns.
  *   - Calls are asynchronous on `stream` (a hipStream_t; NULL = the null
  *     stream).  Results are visible after the stream is synchronised.
- *   - The library allocates no device memory.  Scratch space comes from the
- *     caller as a workspace sized by the *_workspace_size queries.
+ *   - The library allocates no device memory at run time.  Scratch space comes
+ *     from the caller as a workspace sized by the *_workspace_size queries
+ *     (lrqat_backward_static alone uses an array the library holds on each
+ *     GPU).
  *   - Every argument is validated on the host before any HIP call; invalid
  *     arguments return an error status and launch nothing.  A failed launch
  *     returns LRQAT_EHIP.  No C++ exception crosses this interface.
@@ -30,7 +32,7 @@
  *     calling thread.
  *   - Calls that share a workspace must not overlap in time.
  *   - Pointers to tensors read as 16-byte vectors must be 16-byte aligned
- *     (X, Y, dY, dX, Phi0, W_int4, the workspace); A, B, s, dA, dB, ds and
+ *     (X, Y, dY, dX, Phi0, W_int4, the workspace); A, B, s, z, dA, dB, ds and
  *     W0 must be 4-byte aligned.
  */
 #ifndef LRQAT_H
@@ -71,7 +73,7 @@ typedef struct {
   int64_t in_features;   /* k >= 1 */
   int32_t rank;          /* r, 1 <= r <= 256 */
   float alpha;           /* the factor alpha of alpha/r (finite) */
-  int32_t bits;          /* b, see lrqat_phi_format; b <= 4 in this build */
+  int32_t bits;          /* b, see lrqat_phi_format */
   int32_t phi_format;    /* lrqat_phi_format */
   int64_t group_size;    /* 0: one scale per output channel, s[m];
                             g > 0: one scale per row and group of g consecutive
@@ -100,9 +102,17 @@ size_t lrqat_backward_workspace_size(const lrqat_layer* layer, int64_t tokens);
  * INT-b clip(round(W0/s0)).  round() is half-to-even; the quotient and the
  * rounding decision are float32.  s0_out: float32 [m] or [m][k/g];
  * phi0_out: int8 [m][k] or uint8 [m][k/2].
+ *
+ * Asymmetric quantisation (Eq. dequant; the zero offset z is set at range
+ * estimation and frozen, Section 4): with z0_out (int32, shaped like s0) the
+ * range [min(W0, 0), max(W0, 0)] of a row or group maps onto the grid:
+ * s0 = (max - min) / (2^b - 1), z0 = clip(-2^(b-1) - round(min / s0)), and
+ * Phi0 carries the offset, z0 added outside the rounding of the downcast:
+ * fixed point clip(round(2^(8-b) W0/s0) + 2^(8-b) z0), INT-b
+ * clip(round(W0/s0) + z0).  z0_out = NULL: symmetric.
  */
 lrqat_status lrqat_init_from_weights(const lrqat_layer* layer, const float* W0,
-                                     float* s0_out, void* phi0_out, void* stream);
+                                     float* s0_out, int32_t* z0_out, void* phi0_out, void* stream);
 
 /*
  * Forward pass (Section 3, Eq. lr_qat): Y = X_hat * W_hat^T.
@@ -132,12 +142,16 @@ lrqat_status lrqat_forward(const lrqat_layer* layer, int64_t tokens, const void*
  *   dW = dY^T * X_hat,  G = s (.) M (.) dW       (never written to memory)
  *   dA = (alpha/r) G B^T                        float32 [m][r]
  *   dB = (alpha/r) A^T G                        float32 [r][k]
- * M is the clip mask [lo <= round(Phi0 + (alpha/r) A B) <= hi].
- * accumulate = 0 overwrites dA and dB; 1 adds into them (gradient
- * accumulation over micro-batches).  ds (the gradient of the scale) must be
- * NULL in this build.  With T = 0, dA and dB are zeroed (accumulate = 0) or
- * left unchanged.  dA and dB are deterministic: the same inputs give the
- * same bits.
+ *   ds = sum over a row (or row-group) of       float32, shaped like s
+ *        dW (.) (q - z)                         (nullable: skipped when NULL;
+ *                                               the STE gradient of the
+ *                                               learned scale, Section 3)
+ * M is the clip mask [lo <= round(Phi0 + (alpha/r) A B) <= hi] and
+ * q = clip(round(Phi0 + (alpha/r) A B)) the integer grid (z = 0 when NULL).
+ * accumulate = 0 overwrites dA, dB (and ds); 1 adds into them (gradient
+ * accumulation over micro-batches).  With T = 0 they are zeroed
+ * (accumulate = 0) or left unchanged.  dA, dB and ds are deterministic: the
+ * same inputs give the same bits.
  */
 lrqat_status lrqat_backward(const lrqat_layer* layer, int64_t tokens, const void* X,
                             const void* phi0, const float* s, const int32_t* z, const float* A,
@@ -170,11 +184,26 @@ size_t lrqat_backward_static_capacity(void);
  * Merge for inference (Section 3: the adapters fuse into one b-bit integer
  * matrix without loss): W_Z = clip(round(Phi0 + (alpha/r) A B)), written
  * double-packed as uint8 [m][k/2] in the nibble order of
- * LRQAT_PHI_INT_PACKED2; the inference weight is s (.) W_Z.  Needs b <= 4
- * and k even.  No workspace.
+ * LRQAT_PHI_INT_PACKED2; the inference weight is s (.) (W_Z - z).  Needs
+ * b <= 4 and k even.  No workspace.
  */
 lrqat_status lrqat_merge_to_int4(const lrqat_layer* layer, const void* phi0, const float* A,
                                  const float* B, uint8_t* W_int4, void* stream);
+
+/*
+ * Inference on the merged weights (Section 3: after training W_hat = s W_Z,
+ * "without any extra overhead"): Y = X_hat (s (.) (W_Z - z))^T, with W_Z the
+ * packed int4 output of lrqat_merge_to_int4 (layer->bits <= 4; phi_format is
+ * not used), X_hat = X or its per-token int8 fake quantisation when
+ * act_bits = 8 (W4A8), s float32 and z int32 (nullable) shaped like the
+ * layer's scale.  The same GEMM as lrqat_forward without the grid pass.
+ * ws: at least lrqat_infer_workspace_size() bytes (activation codes under
+ * W4A8; a re-laid copy of W_Z when k is not a multiple of 32).
+ */
+size_t lrqat_infer_workspace_size(const lrqat_layer* layer, int64_t tokens);
+lrqat_status lrqat_infer_forward(const lrqat_layer* layer, int64_t tokens, const void* X,
+                                 const uint8_t* W_int4, const float* s, const int32_t* z, void* Y,
+                                 void* ws, size_t ws_bytes, void* stream);
 
 /* Human-readable name of a status code (static string). */
 const char* lrqat_status_string(lrqat_status status);

@@ -509,3 +509,15 @@ def da_rows_abs(L: Layer, X, phi0, s, A, B, dY, rows):
 def db_cols_abs(L: Layer, X, phi0, s, A, B, dY, cols):
     """Columns `cols` of |c| |A|^T |G|."""
     return abs(L.c) * (np.abs(np.asarray(A, np.float64)).T @ _abs_g(L, X, phi0, s, A, B, dY, cols=cols))
+
+
+def ds_rows_abs(L: Layer, X, phi0, s, A, B, dY, rows, z=None):
+    """Rows `rows` of the magnitude of ds's terms: sum over a row (or row-group)
+    of |dW| |q - z|."""
+    q, _, _, _ = grid_from_inputs(phi0, A, B, L.alpha, L.rank, L.bits, L.fmt)
+    Xh = layer_input(X, L.act_bits)
+    dW = np.abs(np.asarray(dY, np.float64)[:, rows].T @ Xh)
+    qz = np.abs(grid_minus_zero(q, z, L.group_size)[rows])
+    if L.group_size == 0:
+        return (dW * qz).sum(axis=1)
+    return (dW * qz).reshape(len(rows), L.k // L.group_size, L.group_size).sum(axis=2)

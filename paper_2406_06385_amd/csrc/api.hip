@@ -1,5 +1,6 @@
 // Host side of the C ABI declared in include/lrqat.h: argument validation,
 // workspace layout and the kernel sequence of each entry point.
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -74,12 +75,13 @@ inline bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintp
 struct Dims {
   int64_t m, k, r, g, ngroups, kpad, mpad;
   int bits, packed, act, bf16;
+  int q8w;  // the integer grid is kept as int8 (fixed-point Phi0 with b = 5..7)
   float c;
   double c64;
 };
 
 struct Workspace {
-  size_t q = 0, mask = 0, n = 0, sx = 0, dA_part = 0, dB_part = 0, G = 0, total = 0;
+  size_t q = 0, mask = 0, n = 0, xh = 0, sx = 0, dA_part = 0, dB_part = 0, ds_part = 0, dW = 0, total = 0;
 };
 
 lrqat_status check_layer(const lrqat_layer* L, Dims& d) {
@@ -93,8 +95,6 @@ lrqat_status check_layer(const lrqat_layer* L, Dims& d) {
     return fail(LRQAT_EINVAL, "unknown phi_format %d", L->phi_format);
   if (L->phi_format == LRQAT_PHI_FIXED_Q8) {
     if (L->bits < 2 || L->bits > 7) return fail(LRQAT_EINVAL, "fixed-point Phi0 needs 2 <= bits <= 7 (got %d)", L->bits);
-    if (L->bits > 4)
-      return fail(LRQAT_EUNSUPPORTED, "bits = %d: this build keeps the integer grid as int4 and runs bits <= 4", L->bits);
   } else {
     if (L->bits < 2 || L->bits > 4) return fail(LRQAT_EINVAL, "packed INT-b Phi0 needs 2 <= bits <= 4 (got %d)", L->bits);
     if (L->in_features % 2) return fail(LRQAT_EINVAL, "packed INT-b Phi0 needs an even in_features");
@@ -104,7 +104,9 @@ lrqat_status check_layer(const lrqat_layer* L, Dims& d) {
     if (L->in_features % L->group_size)
       return fail(LRQAT_EINVAL, "in_features %% group_size != 0 (%lld, %lld)", (long long)L->in_features,
                   (long long)L->group_size);
-    if (L->group_size % 32) return fail(LRQAT_EUNSUPPORTED, "group_size must be a multiple of 32");
+    // a 32-column chunk (the GEMM epilogue's unit of scale, mask and ds work) never straddles two groups
+    if (L->group_size % 32)
+      return fail(LRQAT_EUNSUPPORTED, "group_size must be a multiple of 32 (got %lld)", (long long)L->group_size);
   }
   if (L->act_dtype != LRQAT_FP32 && L->act_dtype != LRQAT_BF16) return fail(LRQAT_EINVAL, "unknown act_dtype");
   if (L->act_bits != 0 && L->act_bits != 8) return fail(LRQAT_EINVAL, "act_bits must be 0 or 8");
@@ -119,6 +121,7 @@ lrqat_status check_layer(const lrqat_layer* L, Dims& d) {
   d.mpad = round_up(d.m, GEMM_BM);
   d.bits = L->bits;
   d.packed = L->phi_format == LRQAT_PHI_INT_PACKED2;
+  d.q8w = !d.packed && d.bits > 4;
   d.act = L->act_bits == 8;
   d.bf16 = L->act_dtype == LRQAT_BF16;
   d.c = L->alpha / float(L->rank);
@@ -126,7 +129,9 @@ lrqat_status check_layer(const lrqat_layer* L, Dims& d) {
   return LRQAT_OK;
 }
 
-Workspace layout(const Dims& d, int64_t T, bool backward) {
+enum Pass { kForward, kBackward, kInfer };
+
+Workspace layout(const Dims& d, int64_t T, Pass pass) {
   Workspace w;
   size_t off = 0;
   auto take = [&](size_t bytes) {
@@ -134,19 +139,25 @@ Workspace layout(const Dims& d, int64_t T, bool backward) {
     off += size_t(round_up(int64_t(bytes), 256));
     return at;
   };
-  w.q = take(size_t(d.m * d.kpad / 2));
-  if (backward) w.mask = take(size_t(d.kpad * d.mpad / 8));
+  if (pass != kInfer) w.q = take(size_t(d.q8w ? d.m * d.kpad : d.m * d.kpad / 2));
+  else if (d.k % 32) w.q = take(size_t(d.m * d.kpad / 2));  // merged weights re-laid with 16-byte aligned rows
+  if (pass == kBackward) w.mask = take(size_t(d.m * (d.kpad / 16) * 2));
   if (d.act) {
-    w.n = take(size_t(T * d.kpad));
-    w.sx = take(size_t(T * 4));
+    if (pass == kBackward) {
+      w.xh = take(size_t(T * d.kpad * 2));  // X_hat in bfloat16 for the dW GEMM
+    } else {
+      w.n = take(size_t(T * d.kpad));
+      w.sx = take(size_t(T * 4));
+    }
   }
-  if (backward) {
+  if (pass == kBackward) {
+    w.ds_part = take(size_t(d.m * (d.kpad / 32) * 4));
     if (d.bf16) {
       const int64_t ntn = (d.k + GEMM_BN - 1) / GEMM_BN, ntm = (d.m + GEMM_BM - 1) / GEMM_BM;
       w.dA_part = take(size_t(ntn * d.m * d.r * 4));
       w.dB_part = take(size_t(ntm * d.r * d.k * 4));
     } else {
-      w.G = take(size_t(d.m * d.k * 4));
+      w.dW = take(size_t(d.m * d.k * 4));
     }
   }
   w.total = off;
@@ -167,10 +178,11 @@ GridArgs grid_args(const Dims& d, const void* phi0, const float* A, const float*
   a.bits = d.bits;
   a.packed = d.packed;
   a.qout = q;
-  a.ldq = d.kpad / 2;
+  a.q8out = d.q8w;
+  a.ldq = d.q8w ? d.kpad : d.kpad / 2;
   a.kq = d.kpad;
   a.mout = mask;
-  a.ldm = d.kpad;
+  a.ldm = d.kpad / 16;
   return a;
 }
 
@@ -191,6 +203,38 @@ lrqat_status hip_status(hipError_t e, const char* what) {
     if (!aligned((ptr), (align))) return fail(LRQAT_EINVAL, "%s is not %d-byte aligned", #ptr, (align)); \
   } while (0)
 
+// Y = X_hat (s (q - z))^T from the integer grid q [m][ldq] (int4 packed, or int8 when d.q8w).
+lrqat_status weight_gemm_forward(const Dims& d, int64_t tokens, const void* X, const uint8_t* q, int64_t ldq,
+                                 const float* s, const int32_t* z, void* Y, uint8_t* base, const Workspace& w,
+                                 hipStream_t st) {
+  if (!d.bf16) {
+    F32Args fa{};
+    fa.T = tokens; fa.m = d.m; fa.k = d.k; fa.r = int(d.r); fa.c = d.c;
+    fa.X = static_cast<const float*>(X);
+    fa.q = q; fa.ldq = ldq; fa.q8 = d.q8w;
+    fa.s = s; fa.z = z; fa.gsize = d.g; fa.ngroups = d.ngroups;
+    return hip_status(timed("f32_fwd", st, [&] { return launch_f32_forward(fa, static_cast<float*>(Y), st); }),
+                      "f32_fwd");
+  }
+  int8_t* n = reinterpret_cast<int8_t*>(base + w.n);
+  float* sx = reinterpret_cast<float*>(base + w.sx);
+  if (d.act)
+    LRQAT_TRY(hip_status(timed("act_quant", st, [&] {
+                           return launch_act_quant(static_cast<const uint16_t*>(X), tokens, d.k, n, d.kpad, nullptr, 0,
+                                                   sx, st);
+                         }), "act_quant"));
+  GemmArgs p{};
+  p.M = tokens; p.N = d.m; p.K = d.k;
+  p.a = d.act ? static_cast<const void*>(n) : X;
+  p.lda = d.act ? d.kpad : d.k;
+  p.b = q; p.ldb = ldq;
+  p.s = s; p.z = z; p.gsize = d.g; p.ngroups = d.ngroups;
+  p.sx = d.act ? sx : nullptr;
+  p.out = Y; p.ldo = d.m;
+  const int opt = (z ? kOptZ : 0) | (d.q8w ? kOptQ8 : 0);
+  return hip_status(timed("gemm_fwd", st, [&] { return launch_gemm(kFwd, d.act, d.g != 0, opt, p, st); }), "gemm_fwd");
+}
+
 }  // namespace
 
 extern "C" {
@@ -202,7 +246,7 @@ size_t lrqat_forward_workspace_size(const lrqat_layer* layer, int64_t tokens) {
     fail(LRQAT_EINVAL, "tokens out of range");
     return 0;
   }
-  return layout(d, tokens, false).total;
+  return layout(d, tokens, kForward).total;
 }
 
 size_t lrqat_backward_workspace_size(const lrqat_layer* layer, int64_t tokens) {
@@ -212,23 +256,25 @@ size_t lrqat_backward_workspace_size(const lrqat_layer* layer, int64_t tokens) {
     fail(LRQAT_EINVAL, "tokens out of range");
     return 0;
   }
-  return layout(d, tokens, true).total;
+  return layout(d, tokens, kBackward).total;
 }
 
-lrqat_status lrqat_init_from_weights(const lrqat_layer* layer, const float* W0, float* s0_out, void* phi0_out,
-                                     void* stream) {
+lrqat_status lrqat_init_from_weights(const lrqat_layer* layer, const float* W0, float* s0_out, int32_t* z0_out,
+                                     void* phi0_out, void* stream) {
   Dims d;
   LRQAT_TRY(check_layer(layer, d));
   NEED(W0, 4);
   NEED(s0_out, 4);
+  if (z0_out && !aligned(z0_out, 4)) return fail(LRQAT_EINVAL, "z0_out is not 4-byte aligned");
   NEED(phi0_out, 16);
   hipStream_t st = static_cast<hipStream_t>(stream);
   const int64_t gsize = d.g ? d.g : d.k;
-  LRQAT_TRY(hip_status(timed("init_scale", st, [&] { return launch_minmax_scale(W0, d.m, d.k, gsize, d.bits, s0_out, st); }),
-                       "init_scale"));
-  LRQAT_TRY(hip_status(timed("init_encode", st,
-                             [&] { return launch_encode(W0, s0_out, d.m, d.k, gsize, d.bits, d.packed, phi0_out, st); }),
-                       "init_encode"));
+  LRQAT_TRY(hip_status(timed("init_scale", st, [&] {
+                         return launch_minmax_scale(W0, d.m, d.k, gsize, d.bits, s0_out, z0_out, st);
+                       }), "init_scale"));
+  LRQAT_TRY(hip_status(timed("init_encode", st, [&] {
+                         return launch_encode(W0, s0_out, z0_out, d.m, d.k, gsize, d.bits, d.packed, phi0_out, st);
+                       }), "init_encode"));
   return LRQAT_OK;
 }
 
@@ -238,16 +284,16 @@ lrqat_status lrqat_forward(const lrqat_layer* layer, int64_t tokens, const void*
   Dims d;
   LRQAT_TRY(check_layer(layer, d));
   if (tokens < 0 || tokens > kMaxDim) return fail(LRQAT_EINVAL, "tokens out of range (%lld)", (long long)tokens);
-  if (z) return fail(LRQAT_EUNSUPPORTED, "the zero offset z is not supported by this build; pass NULL");
   if (tokens == 0) return LRQAT_OK;
   NEED(X, 16);
   NEED(phi0, 16);
   NEED(s, 4);
+  if (z && !aligned(z, 4)) return fail(LRQAT_EINVAL, "z is not 4-byte aligned");
   NEED(A, 4);
   NEED(B, 4);
   NEED(Y, 16);
   NEED(ws, 256);
-  const Workspace w = layout(d, tokens, false);
+  const Workspace w = layout(d, tokens, kForward);
   if (ws_bytes < w.total)
     return fail(LRQAT_EWORKSPACE, "workspace of %zu bytes is smaller than the %zu bytes needed", ws_bytes, w.total);
   hipStream_t st = static_cast<hipStream_t>(stream);
@@ -255,34 +301,7 @@ lrqat_status lrqat_forward(const lrqat_layer* layer, int64_t tokens, const void*
   uint8_t* q = base + w.q;
   const GridArgs ga = grid_args(d, phi0, A, B, q, nullptr);
   LRQAT_TRY(hip_status(timed("grid", st, [&] { return launch_grid(ga, st); }), "grid"));
-
-  if (!d.bf16) {
-    F32Args fa{};
-    fa.T = tokens; fa.m = d.m; fa.k = d.k; fa.r = int(d.r); fa.c = d.c;
-    fa.X = static_cast<const float*>(X);
-    fa.q = q; fa.ldq = d.kpad / 2;
-    fa.s = s; fa.gsize = d.g; fa.ngroups = d.ngroups;
-    LRQAT_TRY(hip_status(timed("f32_fwd", st, [&] { return launch_f32_forward(fa, static_cast<float*>(Y), st); }),
-                         "f32_fwd"));
-    return LRQAT_OK;
-  }
-
-  int8_t* n = reinterpret_cast<int8_t*>(base + w.n);
-  float* sx = reinterpret_cast<float*>(base + w.sx);
-  if (d.act)
-    LRQAT_TRY(hip_status(timed("act_quant", st, [&] {
-                           return launch_act_quant(static_cast<const uint16_t*>(X), tokens, d.k, n, d.kpad, sx, st);
-                         }), "act_quant"));
-  GemmArgs p{};
-  p.M = tokens; p.N = d.m; p.K = d.k;
-  p.a = d.act ? static_cast<const void*>(n) : X;
-  p.lda = d.act ? d.kpad : d.k;
-  p.b = q; p.ldb = d.kpad / 2;
-  p.s = s; p.gsize = d.g; p.ngroups = d.ngroups;
-  p.sx = d.act ? sx : nullptr;
-  p.out = Y; p.ldo = d.m;
-  LRQAT_TRY(hip_status(timed("gemm_fwd", st, [&] { return launch_gemm(kFwd, d.act, d.g != 0, p, st); }), "gemm_fwd"));
-  return LRQAT_OK;
+  return weight_gemm_forward(d, tokens, X, q, ga.ldq, s, z, Y, base, w, st);
 }
 
 }  // extern "C"
@@ -297,15 +316,16 @@ lrqat_status backward_impl(const lrqat_layer* layer, int64_t tokens, const void*
   Dims d;
   LRQAT_TRY(check_layer(layer, d));
   if (tokens < 0 || tokens > kMaxDim) return fail(LRQAT_EINVAL, "tokens out of range (%lld)", (long long)tokens);
-  if (z) return fail(LRQAT_EUNSUPPORTED, "the zero offset z is not supported by this build; pass NULL");
-  if (ds) return fail(LRQAT_EUNSUPPORTED, "the scale gradient ds is not computed by this build; pass NULL");
   if (accumulate != 0 && accumulate != 1) return fail(LRQAT_EINVAL, "accumulate must be 0 or 1");
   NEED(dA, 4);
   NEED(dB, 4);
+  if (ds && !aligned(ds, 4)) return fail(LRQAT_EINVAL, "ds is not 4-byte aligned");
+  if (z && !aligned(z, 4)) return fail(LRQAT_EINVAL, "z is not 4-byte aligned");
   hipStream_t st = static_cast<hipStream_t>(stream);
   if (tokens == 0) {
     LRQAT_TRY(hip_status(launch_reduce(nullptr, 0, d.m * d.r, dA, 0.f, accumulate, st), "reduce"));
     LRQAT_TRY(hip_status(launch_reduce(nullptr, 0, d.r * d.k, dB, 0.f, accumulate, st), "reduce"));
+    if (ds) LRQAT_TRY(hip_status(launch_reduce(nullptr, 0, d.m * d.ngroups, ds, 0.f, accumulate, st), "reduce"));
     return LRQAT_OK;
   }
   NEED(X, 16);
@@ -316,7 +336,7 @@ lrqat_status backward_impl(const lrqat_layer* layer, int64_t tokens, const void*
   NEED(dY, 16);
   if (dX && !aligned(dX, 16)) return fail(LRQAT_EINVAL, "dX is not 16-byte aligned");
   NEED(ws, 256);
-  const Workspace w = layout(d, tokens, true);
+  const Workspace w = layout(d, tokens, kBackward);
   if (ws_bytes < w.total)
     return fail(LRQAT_EWORKSPACE, "workspace of %zu bytes is smaller than the %zu bytes needed", ws_bytes, w.total);
   uint8_t* base = static_cast<uint8_t*>(ws);
@@ -330,45 +350,52 @@ lrqat_status backward_impl(const lrqat_layer* layer, int64_t tokens, const void*
     fa.T = tokens; fa.m = d.m; fa.k = d.k; fa.r = int(d.r); fa.c = d.c;
     fa.X = static_cast<const float*>(X);
     fa.dY = static_cast<const float*>(dY);
-    fa.q = q; fa.ldq = d.kpad / 2;
-    fa.mask = mask; fa.ldm = d.kpad;
-    fa.s = s; fa.gsize = d.g; fa.ngroups = d.ngroups;
+    fa.q = q; fa.ldq = ga.ldq; fa.q8 = d.q8w;
+    fa.mask = mask; fa.ldm = ga.ldm;
+    fa.s = s; fa.z = z; fa.gsize = d.g; fa.ngroups = d.ngroups;
     fa.A = A; fa.B = B;
-    fa.G = reinterpret_cast<float*>(base + w.G);
+    fa.dW = reinterpret_cast<float*>(base + w.dW);
     if (dX)
       LRQAT_TRY(hip_status(timed("f32_dx", st, [&] { return launch_f32_dx(fa, static_cast<float*>(dX), st); }), "f32_dx"));
-    LRQAT_TRY(hip_status(timed("f32_dw", st, [&] { return launch_f32_dw(fa, dA, dB, accumulate, st); }), "f32_dw"));
+    LRQAT_TRY(hip_status(timed("f32_dw", st, [&] { return launch_f32_dw(fa, dA, dB, ds, accumulate, st); }), "f32_dw"));
     return LRQAT_OK;
   }
 
-  int8_t* n = reinterpret_cast<int8_t*>(base + w.n);
-  float* sx = reinterpret_cast<float*>(base + w.sx);
+  // W4A8: the dW GEMM runs on X_hat = s_x n, rounded to bfloat16
+  uint16_t* xh = reinterpret_cast<uint16_t*>(base + w.xh);
   if (d.act)
     LRQAT_TRY(hip_status(timed("act_quant", st, [&] {
-                           return launch_act_quant(static_cast<const uint16_t*>(X), tokens, d.k, n, d.kpad, sx, st);
+                           return launch_act_quant(static_cast<const uint16_t*>(X), tokens, d.k, nullptr, 0, xh,
+                                                   d.kpad, nullptr, st);
                          }), "act_quant"));
   if (dX) {
     GemmArgs p{};
     p.M = tokens; p.N = d.k; p.K = d.m;
     p.a = dY; p.lda = d.m;
-    p.b = q; p.ldb = d.kpad / 2;
-    p.s = s; p.gsize = d.g; p.ngroups = d.ngroups;
+    p.b = q; p.ldb = ga.ldq;
+    p.s = s; p.z = z; p.gsize = d.g; p.ngroups = d.ngroups;
     p.out = dX; p.ldo = d.k;
-    LRQAT_TRY(hip_status(timed("gemm_dx", st, [&] { return launch_gemm(kDx, false, d.g != 0, p, st); }), "gemm_dx"));
+    const int opt = (z ? kOptZ : 0) | (d.q8w ? kOptQ8 : 0);
+    LRQAT_TRY(hip_status(timed("gemm_dx", st, [&] { return launch_gemm(kDx, false, d.g != 0, opt, p, st); }),
+                         "gemm_dx"));
   }
   float* dA_part = reinterpret_cast<float*>(base + w.dA_part);
   float* dB_part = reinterpret_cast<float*>(base + w.dB_part);
+  float* ds_part = reinterpret_cast<float*>(base + w.ds_part);
   GemmArgs p{};
   p.M = d.m; p.N = d.k; p.K = tokens;
   p.a = dY; p.lda = d.m;
-  p.b = d.act ? static_cast<const void*>(n) : X;
+  p.b = d.act ? static_cast<const void*>(xh) : X;
   p.ldb = d.act ? d.kpad : d.k;
-  p.s = s; p.gsize = d.g; p.ngroups = d.ngroups;
-  p.sx = d.act ? sx : nullptr;
-  p.mask = mask; p.ldm = d.kpad;
+  p.s = s; p.z = z; p.gsize = d.g; p.ngroups = d.ngroups;
+  p.mask = mask; p.ldm = ga.ldm;
   p.Am = A; p.Bm = B; p.r = int(d.r);
   p.dA_part = dA_part; p.dB_part = dB_part;
-  LRQAT_TRY(hip_status(timed("gemm_dw", st, [&] { return launch_gemm(kDw, d.act, d.g != 0, p, st); }), "gemm_dw"));
+  if (ds) {
+    p.qd = q; p.ldqd = ga.ldq; p.qd8 = d.q8w;
+    p.ds_part = ds_part; p.ldds = d.kpad / 32;
+  }
+  LRQAT_TRY(hip_status(timed("gemm_dw", st, [&] { return launch_gemm(kDw, false, d.g != 0, 0, p, st); }), "gemm_dw"));
   const int64_t ntn = (d.k + GEMM_BN - 1) / GEMM_BN, ntm = (d.m + GEMM_BM - 1) / GEMM_BM;
   Reduce2Args ra{};
   ra.part[0] = dA_part; ra.nparts[0] = ntn; ra.n[0] = d.m * d.r; ra.out[0] = dA;
@@ -377,6 +404,12 @@ lrqat_status backward_impl(const lrqat_layer* layer, int64_t tokens, const void*
   ra.c = d.c;
   ra.accumulate = accumulate;
   LRQAT_TRY(hip_status(timed("reduce", st, [&] { return launch_reduce2(ra, st); }), "reduce"));
+  if (ds) {
+    const int64_t nchunks = (d.k + 31) / 32, cpg = d.g ? d.g / 32 : nchunks;
+    LRQAT_TRY(hip_status(timed("reduce_ds", st, [&] {
+                           return launch_reduce_ds(ds_part, d.m, d.kpad / 32, nchunks, cpg, d.ngroups, ds, accumulate, st);
+                         }), "reduce_ds"));
+  }
   return LRQAT_OK;
 }
 
@@ -426,7 +459,7 @@ lrqat_status lrqat_backward_static(const lrqat_layer* layer, int64_t tokens, con
   Dims d;
   LRQAT_TRY(check_layer(layer, d));
   if (tokens < 0 || tokens > kMaxDim) return fail(LRQAT_EINVAL, "tokens out of range (%lld)", (long long)tokens);
-  const size_t need = layout(d, tokens, true).total;
+  const size_t need = layout(d, tokens, kBackward).total;
   if (need > kStaticScratchBytes)
     return fail(LRQAT_EWORKSPACE,
                 "lrqat_backward_static: this layer needs %zu bytes of scratch, more than the %zu bytes of the "
@@ -445,6 +478,7 @@ lrqat_status lrqat_merge_to_int4(const lrqat_layer* layer, const void* phi0, con
   Dims d;
   LRQAT_TRY(check_layer(layer, d));
   if (d.k % 2) return fail(LRQAT_EINVAL, "merge_to_int4 needs an even in_features");
+  if (d.bits > 4) return fail(LRQAT_EINVAL, "merge_to_int4 needs bits <= 4 (got %d)", d.bits);
   NEED(phi0, 16);
   NEED(A, 4);
   NEED(B, 4);
@@ -455,6 +489,51 @@ lrqat_status lrqat_merge_to_int4(const lrqat_layer* layer, const void* phi0, con
   ga.kq = d.k;
   LRQAT_TRY(hip_status(timed("merge", st, [&] { return launch_grid(ga, st); }), "merge"));
   return LRQAT_OK;
+}
+
+size_t lrqat_infer_workspace_size(const lrqat_layer* layer, int64_t tokens) {
+  Dims d;
+  if (check_layer(layer, d) != LRQAT_OK) return 0;
+  if (tokens < 0 || tokens > kMaxDim) {
+    fail(LRQAT_EINVAL, "tokens out of range");
+    return 0;
+  }
+  return std::max<size_t>(layout(d, tokens, kInfer).total, 256);
+}
+
+lrqat_status lrqat_infer_forward(const lrqat_layer* layer, int64_t tokens, const void* X, const uint8_t* W_int4,
+                                 const float* s, const int32_t* z, void* Y, void* ws, size_t ws_bytes, void* stream) {
+  Dims d;
+  LRQAT_TRY(check_layer(layer, d));
+  if (d.k % 2) return fail(LRQAT_EINVAL, "merged int4 weights need an even in_features");
+  if (d.bits > 4) return fail(LRQAT_EINVAL, "merged int4 weights need bits <= 4 (got %d)", d.bits);
+  if (tokens < 0 || tokens > kMaxDim) return fail(LRQAT_EINVAL, "tokens out of range (%lld)", (long long)tokens);
+  if (tokens == 0) return LRQAT_OK;
+  NEED(X, 16);
+  NEED(W_int4, 16);
+  NEED(s, 4);
+  if (z && !aligned(z, 4)) return fail(LRQAT_EINVAL, "z is not 4-byte aligned");
+  NEED(Y, 16);
+  NEED(ws, 256);
+  const Workspace w = layout(d, tokens, kInfer);
+  if (ws_bytes < w.total)
+    return fail(LRQAT_EWORKSPACE, "workspace of %zu bytes is smaller than the %zu bytes needed", ws_bytes, w.total);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  uint8_t* base = static_cast<uint8_t*>(ws);
+  Dims di = d;
+  di.q8w = 0;  // merged weights are always packed int4
+  const uint8_t* q = W_int4;
+  int64_t ldq = d.k / 2;
+  if (d.k % 32) {
+    // rows of k/2 bytes are not 16-byte aligned: copy them into zero-padded rows of kpad/2 bytes
+    uint8_t* qp = base + w.q;
+    LRQAT_TRY(hip_status(timed("infer_relayout", st, [&] {
+                           return launch_repack_rows(W_int4, d.m, d.k / 2, qp, d.kpad / 2, st);
+                         }), "infer_relayout"));
+    q = qp;
+    ldq = d.kpad / 2;
+  }
+  return weight_gemm_forward(di, tokens, X, q, ldq, s, z, Y, base, w, st);
 }
 
 const char* lrqat_status_string(lrqat_status status) {

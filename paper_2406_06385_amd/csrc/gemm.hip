@@ -57,18 +57,64 @@ hipError_t launch_reduce2(const Reduce2Args& ra, hipStream_t st) {
   return hipGetLastError();
 }
 
-hipError_t launch_gemm(GemmVariant v, bool act, bool grouped, const GemmArgs& p, hipStream_t st) {
+hipError_t launch_gemm(GemmVariant v, bool act, bool grouped, int opt, const GemmArgs& p, hipStream_t st) {
+  const bool zp = (opt & kOptZ) != 0, i8 = (opt & kOptQ8) != 0;
   switch (v) {
     case kFwd:
-      if (act) return grouped ? launch_fwd_act_grp(p, st) : launch_fwd_act(p, st);
-      return grouped ? launch_fwd_grp(p, st) : launch_fwd(p, st);
+      if (act) return i8 ? launch_fwd_act_i8(grouped, zp, p, st) : launch_fwd_act_i4(grouped, zp, p, st);
+      return i8 ? launch_fwd_i8(grouped, zp, p, st) : launch_fwd_i4(grouped, zp, p, st);
     case kDx:
-      return grouped ? launch_dx_grp(p, st) : launch_dx(p, st);
-    case kDw:
-      if (act) return grouped ? launch_dw_act_grp(p, st) : launch_dw_act(p, st);
-      return grouped ? launch_dw_grp(p, st) : launch_dw(p, st);
+      return i8 ? launch_dx_i8(grouped, zp, p, st) : launch_dx_i4(grouped, zp, p, st);
+    case kDw:  // W4A8 runs the dW GEMM on X_hat in bfloat16
+      if (act) return hipErrorInvalidValue;
+      return grouped ? launch_dw_grp(p, st) : launch_dw_pc(p, st);
   }
   return hipErrorInvalidValue;
+}
+
+// ds[row][grp] = (accumulate ? ds : 0) + the partials of the group's 32-column chunks, summed in
+// chunk order (deterministic).  One thread per (row, group).
+__global__ __launch_bounds__(256) void k_reduce_ds(const float* __restrict__ part, int64_t m, int64_t ldpart,
+                                                   int64_t nchunks, int64_t cpg, int64_t ngroups,
+                                                   float* __restrict__ ds, int accumulate) {
+  const int64_t idx = int64_t(blockIdx.x) * 256 + threadIdx.x;
+  if (idx >= m * ngroups) return;
+  const int64_t row = idx / ngroups, grp = idx % ngroups;
+  const int64_t c0 = grp * cpg, c1 = min(nchunks, c0 + cpg);
+  const float* src = part + row * ldpart;
+  float s0 = 0.f, s1 = 0.f;
+  int64_t c = c0;
+  for (; c + 2 <= c1; c += 2) {
+    s0 += src[c];
+    s1 += src[c + 1];
+  }
+  if (c < c1) s0 += src[c];
+  ds[idx] = (accumulate ? ds[idx] : 0.f) + (s0 + s1);
+}
+
+hipError_t launch_reduce_ds(const float* part, int64_t m, int64_t ldpart, int64_t nchunks, int64_t chunks_per_group,
+                            int64_t ngroups, float* ds, int accumulate, hipStream_t st) {
+  const int64_t n = m * ngroups;
+  if (n == 0) return hipSuccess;
+  k_reduce_ds<<<unsigned((n + 255) / 256), 256, 0, st>>>(part, m, ldpart, nchunks, chunks_per_group, ngroups, ds,
+                                                         accumulate);
+  return hipGetLastError();
+}
+
+// dst[row][0 .. ldd) = src[row][0 .. w) followed by zeros; one thread per destination byte.
+__global__ __launch_bounds__(256) void k_repack_rows(const uint8_t* __restrict__ src, int64_t m, int64_t w,
+                                                     uint8_t* __restrict__ dst, int64_t ldd) {
+  const int64_t idx = int64_t(blockIdx.x) * 256 + threadIdx.x;
+  if (idx >= m * ldd) return;
+  const int64_t row = idx / ldd, col = idx % ldd;
+  dst[idx] = col < w ? src[row * w + col] : uint8_t(0);
+}
+
+hipError_t launch_repack_rows(const uint8_t* src, int64_t m, int64_t w, uint8_t* dst, int64_t ldd, hipStream_t st) {
+  const int64_t n = m * ldd;
+  if (n == 0) return hipSuccess;
+  k_repack_rows<<<unsigned((n + 255) / 256), 256, 0, st>>>(src, m, w, dst, ldd);
+  return hipGetLastError();
 }
 
 hipError_t launch_reduce(const float* part, int64_t nparts, int64_t n, float* out, float c, int accumulate,

@@ -1,9 +1,8 @@
-// Instantiations of the bf16 MFMA GEMM (gemm_impl.h): launch_dw, launch_dw_grp.
+// Instantiations of the bf16 MFMA GEMM (gemm_impl.h): dW GEMM with the G epilogue, per-channel scales.
 #include "gemm_impl.h"
 
 namespace lrqat {
 
-hipError_t launch_dw(const GemmArgs& p, hipStream_t st) { return launch_variant<kDw, false, false>(p, st); }
-hipError_t launch_dw_grp(const GemmArgs& p, hipStream_t st) { return launch_variant<kDw, false, true>(p, st); }
+hipError_t launch_dw_pc(const GemmArgs& p, hipStream_t st) { return launch_variant<kDw, false, false, 0>(p, st); }
 
 }  // namespace lrqat

@@ -1,9 +1,8 @@
-// Instantiations of the bf16 MFMA GEMM (gemm_impl.h): launch_dx, launch_dx_grp.
+// Instantiations of the bf16 MFMA GEMM (gemm_impl.h): dX GEMM, packed int4 grid.
 #include "gemm_impl.h"
 
 namespace lrqat {
 
-hipError_t launch_dx(const GemmArgs& p, hipStream_t st) { return launch_variant<kDx, false, false>(p, st); }
-hipError_t launch_dx_grp(const GemmArgs& p, hipStream_t st) { return launch_variant<kDx, false, true>(p, st); }
+hipError_t launch_dx_i4(bool grouped, bool zp, const GemmArgs& p, hipStream_t st) { return launch_zg<kDx, false, 0>(grouped, zp, p, st); }
 
 }  // namespace lrqat

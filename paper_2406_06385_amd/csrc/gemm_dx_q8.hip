@@ -1,0 +1,8 @@
+// Instantiations of the bf16 MFMA GEMM (gemm_impl.h): dX GEMM, int8 grid (5..7 bits).
+#include "gemm_impl.h"
+
+namespace lrqat {
+
+hipError_t launch_dx_i8(bool grouped, bool zp, const GemmArgs& p, hipStream_t st) { return launch_zg<kDx, false, kOptQ8>(grouped, zp, p, st); }
+
+}  // namespace lrqat

@@ -1,9 +1,8 @@
-// Instantiations of the bf16 MFMA GEMM (gemm_impl.h): launch_fwd, launch_fwd_grp.
+// Instantiations of the bf16 MFMA GEMM (gemm_impl.h): Forward GEMM, packed int4 grid.
 #include "gemm_impl.h"
 
 namespace lrqat {
 
-hipError_t launch_fwd(const GemmArgs& p, hipStream_t st) { return launch_variant<kFwd, false, false>(p, st); }
-hipError_t launch_fwd_grp(const GemmArgs& p, hipStream_t st) { return launch_variant<kFwd, false, true>(p, st); }
+hipError_t launch_fwd_i4(bool grouped, bool zp, const GemmArgs& p, hipStream_t st) { return launch_zg<kFwd, false, 0>(grouped, zp, p, st); }
 
 }  // namespace lrqat

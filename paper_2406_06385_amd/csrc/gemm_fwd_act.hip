@@ -1,9 +1,8 @@
-// Instantiations of the bf16 MFMA GEMM (gemm_impl.h): launch_fwd_act, launch_fwd_act_grp.
+// Instantiations of the bf16 MFMA GEMM (gemm_impl.h): Forward GEMM on int8 activation codes (W4A8), packed int4 grid.
 #include "gemm_impl.h"
 
 namespace lrqat {
 
-hipError_t launch_fwd_act(const GemmArgs& p, hipStream_t st) { return launch_variant<kFwd, true, false>(p, st); }
-hipError_t launch_fwd_act_grp(const GemmArgs& p, hipStream_t st) { return launch_variant<kFwd, true, true>(p, st); }
+hipError_t launch_fwd_act_i4(bool grouped, bool zp, const GemmArgs& p, hipStream_t st) { return launch_zg<kFwd, true, 0>(grouped, zp, p, st); }
 
 }  // namespace lrqat

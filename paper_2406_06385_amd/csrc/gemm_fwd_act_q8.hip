@@ -1,0 +1,8 @@
+// Instantiations of the bf16 MFMA GEMM (gemm_impl.h): Forward GEMM on int8 activation codes, int8 grid.
+#include "gemm_impl.h"
+
+namespace lrqat {
+
+hipError_t launch_fwd_act_i8(bool grouped, bool zp, const GemmArgs& p, hipStream_t st) { return launch_zg<kFwd, true, kOptQ8>(grouped, zp, p, st); }
+
+}  // namespace lrqat

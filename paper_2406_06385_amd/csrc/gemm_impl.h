@@ -6,10 +6,11 @@
 //         epilogue forms G = s * M * dW and the rank-r partial products
 //         G B^T and A^T G (Section 3, STE gradients w.r.t. A and B).
 //
-// W_hat enters as the packed integer grid q written by the grid pass; the
-// operand loaders unpack it into bfloat16 tiles in LDS (exact for |q| <= 8),
-// with the scale s applied in the epilogue (forward, per channel) or folded
-// into the tile (dX, and the forward with group-wise scales).
+// W_hat enters as the integer grid q written by the grid pass (packed int4, or
+// int8 for grids of 5..7 bits); the operand loaders unpack it into bfloat16
+// tiles in LDS (q - z is exact in bfloat16 for |q - z| <= 256), with the scale
+// s applied in the epilogue (forward, per channel) or folded into the tile
+// (dX, and the forward with group-wise scales).
 //
 // Block tile 256 x 256 x 64, four waves in a 2 x 2 arrangement, each wave a
 // 128 x 128 sub-tile of 4 x 4 MFMA 32x32x16 blocks.  Two LDS stages of
@@ -132,15 +133,21 @@ __device__ __forceinline__ void store_kc_i8(uint16_t* tile, const RegsKc8& R) {
   }
 }
 
+// ------------------------------------------------------------------ zero offsets
+// z[row][grp] (z shaped like s; grp = 0 for one offset per row) as an int;
+// rows past the end read 0.
+__device__ __forceinline__ int ld_z(__amdgpu_buffer_rsrc_t rz, int64_t idx) { return int(ld32(rz, uint32_t(idx * 4))); }
+
 // ------------------------------------------------------------------ packed q, K-contiguous (forward B)
 // 256 weight rows x 64 K-values = 256 x 32 bytes; thread t takes 16 bytes
 // (32 values) of rows t/2 and t/2 + 128.  q is zero past column k.
 struct RegsQKc {
   u32x4 v[2];
   float sc[2];
+  int zi[2];
 };
 
-template <bool GRP>
+template <bool GRP, bool ZP>
 __device__ __forceinline__ void load_q_kc(RegsQKc& R, const GemmArgs& p, int64_t row0, int64_t k0) {
   const int t = threadIdx.x;
   const int64_t kk = k0 + 32 * (t & 1);
@@ -148,15 +155,21 @@ __device__ __forceinline__ void load_q_kc(RegsQKc& R, const GemmArgs& p, int64_t
   const uint32_t base = uint32_t((t >> 1) * p.ldb + (kk >> 1)), step = uint32_t(128 * p.ldb);
 #pragma unroll
   for (int i = 0; i < 2; ++i) R.v[i] = ld128(rq, base + i * step);
+  const int64_t grp = GRP ? kk / p.gsize : 0;
   if (GRP) {
     const auto rs = rsrc(p.s + row0 * p.ngroups, (p.N - row0) * p.ngroups * 4);
-    const uint32_t sb = uint32_t(((t >> 1) * p.ngroups + kk / p.gsize) * 4), sstep = uint32_t(128 * p.ngroups * 4);
+    const uint32_t sb = uint32_t(((t >> 1) * p.ngroups + grp) * 4), sstep = uint32_t(128 * p.ngroups * 4);
 #pragma unroll
     for (int i = 0; i < 2; ++i) R.sc[i] = ldf(rs, sb + i * sstep);
   }
+  if (ZP) {
+    const auto rz = rsrc(p.z + row0 * p.ngroups, (p.N - row0) * p.ngroups * 4);
+#pragma unroll
+    for (int i = 0; i < 2; ++i) R.zi[i] = ld_z(rz, ((t >> 1) + 128 * i) * p.ngroups + grp);
+  }
 }
 
-template <bool GRP>
+template <bool GRP, bool ZP>
 __device__ __forceinline__ void store_q_kc(uint16_t* tile, const RegsQKc& R) {
   const int t = threadIdx.x;
 #pragma unroll
@@ -168,7 +181,12 @@ __device__ __forceinline__ void store_q_kc(uint16_t* tile, const RegsQKc& R) {
       u32x4 o;
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        float a = float(nibble(w, 2 * q)), b = float(nibble(w, 2 * q + 1));
+        int na = nibble(w, 2 * q), nb = nibble(w, 2 * q + 1);
+        if (ZP) {
+          na -= R.zi[i];
+          nb -= R.zi[i];
+        }
+        float a = float(na), b = float(nb);
         if (GRP) {
           a *= R.sc[i];
           b *= R.sc[i];
@@ -177,6 +195,60 @@ __device__ __forceinline__ void store_q_kc(uint16_t* tile, const RegsQKc& R) {
       }
       *reinterpret_cast<u32x4*>(tile + tile_off(row, 4 * (t & 1) + c)) = o;
     }
+  }
+}
+
+// ------------------------------------------------------------------ int8 q, K-contiguous (forward B, 5..7-bit grids)
+// 256 weight rows x 64 bytes: thread t loads 8 bytes of rows t/8 + 32 i; q is zero past column k.
+struct RegsQKc8 {
+  u32x2 v[8];
+  float sc[8];
+  int zi[8];
+};
+
+template <bool GRP, bool ZP>
+__device__ __forceinline__ void load_q_kc8(RegsQKc8& R, const GemmArgs& p, int64_t row0, int64_t k0) {
+  const int t = threadIdx.x;
+  const auto rq = rsrc(static_cast<const uint8_t*>(p.b) + row0 * p.ldb, (p.N - row0) * p.ldb);
+  const int64_t kk = k0 + 8 * (t & 7);
+  const uint32_t base = uint32_t((t >> 3) * p.ldb + kk), step = uint32_t(32 * p.ldb);
+#pragma unroll
+  for (int i = 0; i < 8; ++i) R.v[i] = ld64(rq, base + i * step);
+  const int64_t grp = GRP ? kk / p.gsize : 0;
+  if (GRP) {
+    const auto rs = rsrc(p.s + row0 * p.ngroups, (p.N - row0) * p.ngroups * 4);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) R.sc[i] = ldf(rs, uint32_t((((t >> 3) + 32 * i) * p.ngroups + grp) * 4));
+  }
+  if (ZP) {
+    const auto rz = rsrc(p.z + row0 * p.ngroups, (p.N - row0) * p.ngroups * 4);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) R.zi[i] = ld_z(rz, ((t >> 3) + 32 * i) * p.ngroups + grp);
+  }
+}
+
+template <bool GRP, bool ZP>
+__device__ __forceinline__ void store_q_kc8(uint16_t* tile, const RegsQKc8& R) {
+  const int t = threadIdx.x;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    u32x4 o;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const uint32_t w = R.v[i][q >> 1];
+      int na = sbyte(w, 2 * (q & 1)), nb = sbyte(w, 2 * (q & 1) + 1);
+      if (ZP) {
+        na -= R.zi[i];
+        nb -= R.zi[i];
+      }
+      float a = float(na), b = float(nb);
+      if (GRP) {
+        a *= R.sc[i];
+        b *= R.sc[i];
+      }
+      o[q] = pack_bf16x2(a, b);
+    }
+    *reinterpret_cast<u32x4*>(tile + tile_off((t >> 3) + 32 * i, t & 7)) = o;
   }
 }
 
@@ -193,9 +265,37 @@ __device__ __forceinline__ void store_q_kc(uint16_t* tile, const RegsQKc& R) {
 struct RegsQKs {
   uint32_t w[8];
   float sc[8];
+  int zi[8];
 };
 
-template <bool GRP>
+// Scales (and zero offsets) of the 8 K-lines (weight rows) k0 + 8 kg .. +7 at column col.
+template <bool GRP, bool ZP>
+__device__ __forceinline__ void load_ks_scales(float (&sc)[8], int (&zi)[8], const GemmArgs& p, int64_t k0, int kg,
+                                               int64_t col) {
+  const int64_t grp = GRP ? col / p.gsize : 0;
+  if (GRP) {
+    const auto rs = rsrc(p.s + k0 * p.ngroups, (p.K - k0) * p.ngroups * 4);
+    const uint32_t sb = uint32_t((8 * kg * p.ngroups + grp) * 4), sstep = uint32_t(p.ngroups * 4);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) sc[e] = ldf(rs, sb + e * sstep);
+  } else {
+    // the 8 rows' scales are consecutive: two 16-byte loads (rows past K read as zeros)
+    const auto rs = rsrc(p.s + k0, (p.K - k0) * 4);
+    const u32x4 s0 = ld128(rs, uint32_t(8 * kg * 4)), s1 = ld128(rs, uint32_t((8 * kg + 4) * 4));
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      sc[e] = __uint_as_float(s0[e]);
+      sc[4 + e] = __uint_as_float(s1[e]);
+    }
+  }
+  if (ZP) {
+    const auto rz = rsrc(p.z + k0 * p.ngroups, (p.K - k0) * p.ngroups * 4);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) zi[e] = ld_z(rz, (8 * kg + e) * p.ngroups + grp);
+  }
+}
+
+template <bool GRP, bool ZP>
 __device__ __forceinline__ void load_q_ks(RegsQKs& R, const GemmArgs& p, int64_t n0, int64_t k0) {
   const int t = threadIdx.x;
   const int kg = t & 7, a = t >> 3;
@@ -204,23 +304,10 @@ __device__ __forceinline__ void load_q_ks(RegsQKs& R, const GemmArgs& p, int64_t
   const uint32_t base = uint32_t(8 * kg * p.ldb + (col >> 1)), step = uint32_t(p.ldb);
 #pragma unroll
   for (int e = 0; e < 8; ++e) R.w[e] = ld32(rq, base + e * step);
-  if (GRP) {
-    const auto rs = rsrc(p.s + k0 * p.ngroups, (p.K - k0) * p.ngroups * 4);
-    const uint32_t sb = uint32_t((8 * kg * p.ngroups + col / p.gsize) * 4), sstep = uint32_t(p.ngroups * 4);
-#pragma unroll
-    for (int e = 0; e < 8; ++e) R.sc[e] = ldf(rs, sb + e * sstep);
-  } else {
-    // the 8 rows' scales are consecutive: two 16-byte loads (rows past K read as zeros)
-    const auto rs = rsrc(p.s + k0, (p.K - k0) * 4);
-    const u32x4 s0 = ld128(rs, uint32_t(8 * kg * 4)), s1 = ld128(rs, uint32_t((8 * kg + 4) * 4));
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      R.sc[e] = __uint_as_float(s0[e]);
-      R.sc[4 + e] = __uint_as_float(s1[e]);
-    }
-  }
+  load_ks_scales<GRP, ZP>(R.sc, R.zi, p, k0, kg, col);
 }
 
+template <bool ZP>
 __device__ __forceinline__ void store_q_ks(uint16_t* tile, const RegsQKs& R) {
   const int t = threadIdx.x;
   const int kg = t & 7, a = t >> 3;
@@ -228,9 +315,53 @@ __device__ __forceinline__ void store_q_ks(uint16_t* tile, const RegsQKs& R) {
   for (int c = 0; c < 8; ++c) {
     u32x4 o;
 #pragma unroll
-    for (int q = 0; q < 4; ++q)
-      o[q] = pack_bf16x2(float(nibble(R.w[2 * q], c)) * R.sc[2 * q],
-                         float(nibble(R.w[2 * q + 1], c)) * R.sc[2 * q + 1]);
+    for (int q = 0; q < 4; ++q) {
+      int na = nibble(R.w[2 * q], c), nb = nibble(R.w[2 * q + 1], c);
+      if (ZP) {
+        na -= R.zi[2 * q];
+        nb -= R.zi[2 * q + 1];
+      }
+      o[q] = pack_bf16x2(float(na) * R.sc[2 * q], float(nb) * R.sc[2 * q + 1]);
+    }
+    *reinterpret_cast<u32x4*>(tile + tile_off(8 * a + c, kg)) = o;
+  }
+}
+
+// int8 q (dX B, 5..7-bit grids): 8 bytes (columns 8a .. 8a + 7) of each K-line.
+struct RegsQKs8 {
+  u32x2 v[8];
+  float sc[8];
+  int zi[8];
+};
+
+template <bool GRP, bool ZP>
+__device__ __forceinline__ void load_q_ks8(RegsQKs8& R, const GemmArgs& p, int64_t n0, int64_t k0) {
+  const int t = threadIdx.x;
+  const int kg = t & 7, a = t >> 3;
+  const int64_t col = n0 + 8 * a;
+  const auto rq = rsrc(static_cast<const uint8_t*>(p.b) + k0 * p.ldb, (p.K - k0) * p.ldb);
+  const uint32_t base = uint32_t(8 * kg * p.ldb + col), step = uint32_t(p.ldb);
+#pragma unroll
+  for (int e = 0; e < 8; ++e) R.v[e] = ld64(rq, base + e * step);
+  load_ks_scales<GRP, ZP>(R.sc, R.zi, p, k0, kg, col);
+}
+
+template <bool ZP>
+__device__ __forceinline__ void store_q_ks8(uint16_t* tile, const RegsQKs8& R) {
+  const int t = threadIdx.x;
+  const int kg = t & 7, a = t >> 3;
+#pragma unroll
+  for (int c = 0; c < 8; ++c) {
+    u32x4 o;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      int na = sbyte(R.v[2 * q][c >> 2], c & 3), nb = sbyte(R.v[2 * q + 1][c >> 2], c & 3);
+      if (ZP) {
+        na -= R.zi[2 * q];
+        nb -= R.zi[2 * q + 1];
+      }
+      o[q] = pack_bf16x2(float(na) * R.sc[2 * q], float(nb) * R.sc[2 * q + 1]);
+    }
     *reinterpret_cast<u32x4*>(tile + tile_off(8 * a + c, kg)) = o;
   }
 }
@@ -266,88 +397,58 @@ __device__ __forceinline__ void store_ks_bf16(uint16_t* tile, const RegsKs& R) {
   }
 }
 
-// int8 codes n [T][ld] times s_x[t] (dW B under W4A8).
-struct RegsKs8 {
-  u32x2 v[8];
-  float sx[8];
-};
-
-__device__ __forceinline__ void load_ks_i8(RegsKs8& R, const int8_t* __restrict__ src, int64_t ld,
-                                           const float* __restrict__ sx, int64_t c0, int64_t k0, int64_t K) {
-  const int t = threadIdx.x;
-  const int kg = t & 7, a = t >> 3;
-  const auto r = rsrc(src + k0 * ld + c0, (K - k0) * ld - c0);
-  const auto rs = rsrc(sx + k0, (K - k0) * 4);
-  const uint32_t base = uint32_t(8 * kg * ld + 8 * a), step = uint32_t(ld);
-#pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    R.v[e] = ld64(r, base + e * step);
-    R.sx[e] = ldf(rs, uint32_t((8 * kg + e) * 4));
-  }
-}
-
-__device__ __forceinline__ void store_ks_i8(uint16_t* tile, const RegsKs8& R) {
-  const int t = threadIdx.x;
-  const int kg = t & 7, a = t >> 3;
-#pragma unroll
-  for (int c = 0; c < 8; ++c) {
-    u32x4 o;
-#pragma unroll
-    for (int q = 0; q < 4; ++q)
-      o[q] = pack_bf16x2(float(sbyte(R.v[2 * q][c >> 2], c & 3)) * R.sx[2 * q],
-                         float(sbyte(R.v[2 * q + 1][c >> 2], c & 3)) * R.sx[2 * q + 1]);
-    *reinterpret_cast<u32x4*>(tile + tile_off(8 * a + c, kg)) = o;
-  }
-}
-
 // ------------------------------------------------------------------ the kernel
 
-template <int V, bool ACT, bool GRP, bool VEC>
+template <int V, bool ACT, bool GRP, bool VEC, int OPT>
 struct Loader;
 
-template <bool ACT, bool GRP, bool VEC>
-struct Loader<kFwd, ACT, GRP, VEC> {
+template <bool ACT, bool GRP, bool VEC, int OPT>
+struct Loader<kFwd, ACT, GRP, VEC, OPT> {
+  static constexpr bool ZP = (OPT & kOptZ) != 0, Q8 = (OPT & kOptQ8) != 0;
   typename std::conditional<ACT, RegsKc8, RegsKc>::type ra;
-  RegsQKc rb;
+  typename std::conditional<Q8, RegsQKc8, RegsQKc>::type rb;
   __device__ __forceinline__ void load(const GemmArgs& p, int64_t m0, int64_t n0, int64_t k0) {
     if constexpr (ACT) load_kc_i8(ra, static_cast<const int8_t*>(p.a), p.lda, m0, p.M, k0);
     else load_kc_bf16<VEC>(ra, static_cast<const uint16_t*>(p.a), p.lda, m0, p.M, k0, p.K);
-    load_q_kc<GRP>(rb, p, n0, k0);
+    if constexpr (Q8) load_q_kc8<GRP, ZP>(rb, p, n0, k0);
+    else load_q_kc<GRP, ZP>(rb, p, n0, k0);
   }
   __device__ __forceinline__ void store(const GemmArgs& p, uint16_t* As, uint16_t* Bs) {
     if constexpr (ACT) store_kc_i8(As, ra);
     else store_kc<VEC>(As, ra, p.K);
-    store_q_kc<GRP>(Bs, rb);
+    if constexpr (Q8) store_q_kc8<GRP, ZP>(Bs, rb);
+    else store_q_kc<GRP, ZP>(Bs, rb);
   }
 };
 
-template <bool ACT, bool GRP, bool VEC>
-struct Loader<kDx, ACT, GRP, VEC> {
+template <bool ACT, bool GRP, bool VEC, int OPT>
+struct Loader<kDx, ACT, GRP, VEC, OPT> {
+  static constexpr bool ZP = (OPT & kOptZ) != 0, Q8 = (OPT & kOptQ8) != 0;
   RegsKc ra;
-  RegsQKs rb;
+  typename std::conditional<Q8, RegsQKs8, RegsQKs>::type rb;
   __device__ __forceinline__ void load(const GemmArgs& p, int64_t m0, int64_t n0, int64_t k0) {
     load_kc_bf16<VEC>(ra, static_cast<const uint16_t*>(p.a), p.lda, m0, p.M, k0, p.K);
-    load_q_ks<GRP>(rb, p, n0, k0);
+    if constexpr (Q8) load_q_ks8<GRP, ZP>(rb, p, n0, k0);
+    else load_q_ks<GRP, ZP>(rb, p, n0, k0);
   }
   __device__ __forceinline__ void store(const GemmArgs& p, uint16_t* As, uint16_t* Bs) {
     store_kc<VEC>(As, ra, p.K);
-    store_q_ks(Bs, rb);
+    if constexpr (Q8) store_q_ks8<ZP>(Bs, rb);
+    else store_q_ks<ZP>(Bs, rb);
   }
 };
 
-template <bool ACT, bool GRP, bool VEC>
-struct Loader<kDw, ACT, GRP, VEC> {
-  RegsKs ra;
-  typename std::conditional<ACT, RegsKs8, RegsKs>::type rb;
+template <bool ACT, bool GRP, bool VEC, int OPT>
+struct Loader<kDw, ACT, GRP, VEC, OPT> {
+  static_assert(!ACT, "the dW GEMM reads bfloat16 operands (W4A8: X_hat)");
+  RegsKs ra, rb;
   __device__ __forceinline__ void load(const GemmArgs& p, int64_t m0, int64_t n0, int64_t k0) {
     load_ks_bf16<VEC>(ra, static_cast<const uint16_t*>(p.a), p.lda, m0, k0, p.K);
-    if constexpr (ACT) load_ks_i8(rb, static_cast<const int8_t*>(p.b), p.ldb, p.sx, n0, k0, p.K);
-    else load_ks_bf16<VEC>(rb, static_cast<const uint16_t*>(p.b), p.ldb, n0, k0, p.K);
+    load_ks_bf16<VEC>(rb, static_cast<const uint16_t*>(p.b), p.ldb, n0, k0, p.K);
   }
   __device__ __forceinline__ void store(const GemmArgs&, uint16_t* As, uint16_t* Bs) {
     store_ks_bf16(As, ra);
-    if constexpr (ACT) store_ks_i8(Bs, rb);
-    else store_ks_bf16(Bs, rb);
+    store_ks_bf16(Bs, rb);
   }
 };
 
@@ -418,7 +519,7 @@ __device__ __forceinline__ void tile_of(int64_t b, int64_t ntm, int64_t ntn, int
   tn = off / gm;
 }
 
-template <int V, bool ACT, bool GRP, bool VEC>
+template <int V, bool ACT, bool GRP, bool VEC, int OPT>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void k_gemm(GemmArgs p) {
   // A stages 0, 1 then B stages 0, 1 (128 KiB); the dW epilogue reuses all
   // of it for G.
@@ -444,14 +545,15 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   // kt+1 held in one set is written to the other stage and the tile kt+2
   // is fetched into the other set.  Loads past the last tile read zeros or
   // unused data and are never consumed, so the body has no branches.
-  Loader<V, ACT, GRP, VEC> L0, L1;
+  using Ld = Loader<V, ACT, GRP, VEC, OPT>;
+  Ld L0, L1;
   const int nk = int((p.K + BK - 1) / BK);
   L0.load(p, m0, n0, 0);
   L1.load(p, m0, n0, BK);
   L0.store(p, lds, lds + 2 * TILE);
   __syncthreads();
 
-  auto step = [&](int kt, Loader<V, ACT, GRP, VEC>& Lnext, Loader<V, ACT, GRP, VEC>& Lfree) {
+  auto step = [&](int kt, Ld& Lnext, Ld& Lfree) {
     const uint16_t* As = lds + (kt & 1) * TILE;
     const uint16_t* Bs = lds + (2 + (kt & 1)) * TILE;
     const int nx = (kt + 1) & 1;
@@ -471,12 +573,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
 #pragma unroll
       for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          // forward / dX: D = B-tile x A-tile^T, so a lane's accumulator holds 4
-          // consecutive output columns of one output row (8-byte stores)
-          if constexpr (V == kDw) acc[i][j] = mfma32(fa[s & 1][i], fb[s & 1][j], acc[i][j]);
-          else acc[i][j] = mfma32(fb[s & 1][j], fa[s & 1][i], acc[i][j]);
-        }
+        for (int j = 0; j < 4; ++j)
+          // D = B-tile x A-tile^T: a lane's accumulator holds 4 consecutive output
+          // columns of one output row (8-byte stores; dW: 4 columns of one weight row)
+          acc[i][j] = mfma32(fb[s & 1][j], fa[s & 1][i], acc[i][j]);
     }
     Lnext.store(p, lds + nx * TILE, lds + (2 + nx) * TILE);
     interleave();
@@ -489,8 +589,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   }
   if (kt < nk) step(kt, L1, L0);
 
+  // acc[i][j][4g + e] = C[m0 + wm + 32 i + lane % 32][n0 + wn + 32 j + 8 g + 4 (lane / 32) + e]
   if constexpr (V == kFwd || V == kDx) {
-    // acc[i][j][4g + e] = C[m0 + wm + 32 i + lane % 32][n0 + wn + 32 j + 8 g + 4 (lane / 32) + e]
     uint16_t* out = static_cast<uint16_t*>(p.out);
     const int64_t row_l = m0 + wm + (lane & 31);
     const int64_t col_l = n0 + wn + 4 * (lane >> 5);
@@ -528,65 +628,115 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
         }
     }
   } else {
-    // ---- dW epilogue: G = s * M * dW staged in LDS (bf16, transposed), then both
+    // ---- dW epilogue: G = s * M * dW staged in LDS as bf16 [row][col], then both
     // rank-r products from LDS; the accumulators are dead once G is staged.
-    // Accumulator layout: acc[i][j][v] = dW[m0 + wm + 32 i + acc_row(v)][n0 + wn + 32 j + lane % 32].
+    // The lane holds rows R_i = m0 + wm + 32 i + lane % 32 and, in chunk j (32
+    // columns from n0 + wn + 32 j), the columns 8 g + 4 h + e (h = lane / 32).
     const int r = p.r;
     const int nrb = (r + 31) / 32;
     const int half = lane >> 5;
-    const int64_t rowb = m0 + wm;  // first row of the wave
+    const int lrow = wm + (lane & 31);  // local row of i = 0
     uint16_t* Gs = lds;
 
-    // clip-mask bits of the lane's four columns over the wave's 128 rows: word i
-    // holds rows 32 i .. +31 (two 16-row words of the mask)
-    u32x4 mbits[4];
+    // columns of chunk j inside N, as a 32-bit mask over the chunk
+    uint32_t colok[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const int64_t col = n0 + wn + 32 * j + (lane & 31);
-      // unconditional 2-byte buffer loads (no branch around a load); columns >= N are dropped
-      const auto rm = rsrc(p.mask + (rowb >> 4) * p.ldm, 8 * p.ldm * 2);
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const uint32_t w = ld16(rm, uint32_t((2 * i * p.ldm + col) * 2)) |
-                           (ld16(rm, uint32_t(((2 * i + 1) * p.ldm + col) * 2)) << 16);
-        mbits[j][i] = col < p.N ? w : 0u;
-      }
+      const int64_t left = p.N - (n0 + wn + 32 * j);
+      colok[j] = left >= 32 ? 0xFFFFFFFFu : left <= 0 ? 0u : (1u << left) - 1u;
     }
-    const auto rsg = rsrc(p.s + m0 * p.ngroups, (p.M - m0) * p.ngroups * 4);  // group-wise scales of the block's rows
+    // clip-mask bits of chunk j of row R_i: two adjacent 16-bit words, one 4-byte load (rows >= M read 0)
+    uint32_t mw[4][4];
+    {
+      const auto rm = rsrc(p.mask + (m0 + wm) * p.ldm, (p.M - m0 - wm) * p.ldm * 2);
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int64_t word = (((lane & 31) + 32 * i) * p.ldm + ((n0 + wn + 32 * j) >> 4)) * 2;
+          mw[i][j] = ld32(rm, uint32_t(word)) & colok[j];
+        }
+    }
+    // scales: per channel through LDS, group-wise per (row, chunk) (groups hold whole chunks)
+    const auto rsg = rsrc(p.s + m0 * p.ngroups, (p.M - m0) * p.ngroups * 4);  // rows >= M read 0
     if constexpr (!GRP) {
-      s_tile[threadIdx.x] = ldf(rsg, uint32_t(threadIdx.x * 4));  // rows >= M read 0
+      s_tile[threadIdx.x] = ldf(rsg, uint32_t(threadIdx.x * 4));
       __syncthreads();
     }
+    float sc[4][4];
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int g4 = 0; g4 < 4; ++g4) {
-        // scales of the 4 consecutive rows 32 i + 8 g4 + 4 half .. +3 of the wave
-        const int lr = wm + 32 * i + 8 * g4 + 4 * half;
-        f32x4 sc4 = {0.f, 0.f, 0.f, 0.f};
-        if constexpr (!GRP) sc4 = *reinterpret_cast<const f32x4*>(&s_tile[lr]);
-        // rows lr .. lr + 3 inside M (the padded mask rows past m are not written by the grid pass)
-        const int64_t rows_in = p.M - m0 - lr;
-        const uint32_t rowbits = rows_in >= 4 ? 15u : rows_in <= 0 ? 0u : (1u << rows_in) - 1u;
+      for (int j = 0; j < 4; ++j) {
+        if constexpr (GRP)
+          sc[i][j] = ldf(rsg, uint32_t(((lrow + 32 * i) * p.ngroups + (n0 + wn + 32 * j) / p.gsize) * 4));
+        else
+          sc[i][j] = s_tile[lrow + 32 * i];
+      }
+
+    // scale-gradient partials: ds_part[R_i][chunk] = sum over the chunk of dW (q - z); the lane
+    // sums its 16 columns, the lane 32 apart the other 16
+    if (p.ds_part) {
+      const auto rq = rsrc(p.qd + (m0 + wm) * p.ldqd, (p.M - m0 - wm) * p.ldqd);  // rows >= M read 0
+      // without a zero offset the resource is empty and every z reads 0
+      const auto rz = p.z ? rsrc(p.z + (m0 + wm) * p.ngroups, (p.M - m0 - wm) * p.ngroups * 4) : rsrc(p.ds_part, 0);
+      const auto rd = rsrc(p.ds_part + (m0 + wm) * p.ldds, (p.M - m0 - wm) * p.ldds * 4);
+      const bool q8 = p.qd8 != 0;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int rl = (lane & 31) + 32 * i;  // row relative to m0 + wm
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          const int lj = wn + 32 * j + (lane & 31);
-          const int64_t col = n0 + lj;
-          // the 4 rows' clip-mask bits (acc_row of element 4 g4 + e is 8 g4 + 4 half + e);
-          // columns past N have a zero mask word
-          const uint32_t bits = (mbits[j][i] >> (8 * g4 + 4 * half)) & rowbits;
-          float g[4];
+          const int64_t c0 = n0 + wn + 32 * j;
+          const int zi = ld_z(rz, int64_t(rl) * p.ngroups + (GRP ? c0 / p.gsize : 0));
+          float sum = 0.f;
+          if (q8) {
+            // bytes c0 .. c0 + 31 of the row; column 8 g + 4 h + e is byte e of word 2 g + h
+            const u32x4 qa = ld128(rq, uint32_t(rl * p.ldqd + c0)), qb = ld128(rq, uint32_t(rl * p.ldqd + c0 + 16));
 #pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            float sc;
-            if constexpr (GRP) sc = ldf(rsg, uint32_t(((lr + e) * p.ngroups + col / p.gsize) * 4));  // rows >= M read 0
-            else sc = sc4[e];
-            g[e] = (bits >> e) & 1u ? acc[i][j][4 * g4 + e] * sc : 0.f;
+            for (int g = 0; g < 4; ++g) {
+              const uint32_t w = (2 * g + half) < 4 ? qa[(2 * g + half) & 3] : qb[(2 * g + half) & 3];
+#pragma unroll
+              for (int e = 0; e < 4; ++e) {
+                const bool ok = (colok[j] >> (8 * g + 4 * half + e)) & 1u;
+                sum = __builtin_fmaf(ok ? acc[i][j][4 * g + e] : 0.f, float(sbyte(w, e) - zi), sum);
+              }
+            }
+          } else {
+            // nibbles c0 .. c0 + 31 of the row: column 8 g + 4 h + e is nibble 4 h + e of word g
+            const u32x4 qv = ld128(rq, uint32_t(rl * p.ldqd + (c0 >> 1)));
+#pragma unroll
+            for (int g = 0; g < 4; ++g)
+#pragma unroll
+              for (int e = 0; e < 4; ++e) {
+                const bool ok = (colok[j] >> (8 * g + 4 * half + e)) & 1u;
+                sum = __builtin_fmaf(ok ? acc[i][j][4 * g + e] : 0.f, float(nibble(qv[g], 4 * half + e) - zi), sum);
+              }
           }
-          // G is staged transposed, Gs[j][i]: the lane's 4 consecutive rows are one 8-byte write
-          *reinterpret_cast<u32x2*>(Gs + g_off(lj, lr)) = u32x2{pack_bf16x2(g[0], g[1]), pack_bf16x2(g[2], g[3])};
+          sum += __shfl_xor(sum, 32);
+          if (half == 0 && colok[j])
+            __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(sum), rd,
+                                                  int(uint32_t((rl * p.ldds + (c0 >> 5)) * 4)), 0, 0);
         }
       }
+    }
+
+    // G staged as Gs[row][col]: the lane's 4 consecutive columns are one 8-byte write
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int lr = lrow + 32 * i;
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const uint32_t bits = mw[i][j] >> (8 * g + 4 * half);
+          float gv[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) gv[e] = (bits >> e) & 1u ? acc[i][j][4 * g + e] * sc[i][j] : 0.f;
+          *reinterpret_cast<u32x2*>(Gs + g_off(lr, wn + 32 * j + 8 * g + 4 * half)) =
+              u32x2{pack_bf16x2(gv[0], gv[1]), pack_bf16x2(gv[2], gv[3])};
+        }
+    }
 
     // stage rank block rb of A (transposed) or B as bf16 [32][256] in `rt_tile`
     auto stage = [&](const float* __restrict__ src, bool is_a, int rb) {
@@ -624,7 +774,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
       __syncthreads();  // G staged / previous rank block consumed
       stage(p.Am, true, rb);
       __syncthreads();
-      // dB: A operand = A^T rows (rt_tile), B operand = 8 consecutive rows of a G column (one read)
+      // dB: A operand = A^T rows (rt_tile), B operand = 8 consecutive rows of a G column (LDS transpose loads)
 #pragma unroll
       for (int cb2 = 0; cb2 < 2; ++cb2) {
         const int cb = 2 * wave + cb2;            // column block of 32
@@ -634,9 +784,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
         for (int v = 0; v < 16; ++v) d[v] = 0.f;
 #pragma unroll 4
         for (int s2 = 0; s2 < 16; ++s2) {
-          const int ib = 16 * s2 + 8 * half;
-          const u32x4 aa = *reinterpret_cast<const u32x4*>(&rt_tile[g_off(lane & 31, ib)]);
-          const u32x4 gb = *reinterpret_cast<const u32x4*>(Gs + g_off(lj, ib));  // G[ib .. ib + 7][lj]
+          const u32x4 aa = *reinterpret_cast<const u32x4*>(&rt_tile[g_off(lane & 31, 16 * s2 + 8 * half)]);
+          const u32x4 gb = frag_tr_g(Gs, 32 * cb, 16 * s2, lane);  // G[16 s2 + 8 half .. +7][32 cb + l % 32]
           d = mfma32(aa, gb, d);
         }
         if (n0 + lj < p.N) {
@@ -651,7 +800,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
       __syncthreads();
       stage(p.Bm, false, rb);
       __syncthreads();
-      // dA: A operand = G rows (transpose loads), B operand = B rows (rt_tile)
+      // dA: A operand = 8 consecutive columns of a G row (one read), B operand = B rows (rt_tile)
 #pragma unroll
       for (int h2 = 0; h2 < 2; ++h2) {
         const int rowblk = 2 * wave + h2;
@@ -660,7 +809,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
         for (int v = 0; v < 16; ++v) d[v] = 0.f;
 #pragma unroll 4
         for (int s2 = 0; s2 < 16; ++s2) {
-          const u32x4 ga = frag_tr_g(Gs, 32 * rowblk, 16 * s2, lane);  // G[32 rowblk + l % 32][16 s2 + 8 half .. +7]
+          const u32x4 ga = *reinterpret_cast<const u32x4*>(Gs + g_off(32 * rowblk + (lane & 31), 16 * s2 + 8 * half));
           const u32x4 bb = *reinterpret_cast<const u32x4*>(&rt_tile[g_off(lane & 31, 16 * s2 + 8 * half)]);
           d = mfma32(ga, bb, d);
         }
@@ -677,15 +826,23 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
 }
 
 // Launch one instantiation (all variants share this helper).
-template <int V, bool ACT, bool GRP>
+template <int V, bool ACT, bool GRP, int OPT>
 hipError_t launch_variant(const GemmArgs& p, hipStream_t st) {
   const int64_t ntm = (p.M + BM - 1) / BM, ntn = (p.N + BN - 1) / BN;
   // fast path: 16-byte row vectors (leading dimensions multiples of 8
   // elements) and, for K-contiguous operands, no partial last K-tile
   const bool vec = (p.lda % 8 == 0) && (V != kDw || p.ldb % 8 == 0) && (V == kDw || p.K % BK == 0);
-  if (vec) k_gemm<V, ACT, GRP, true><<<unsigned(ntm * ntn), 256, 0, st>>>(p);
-  else k_gemm<V, ACT, GRP, false><<<unsigned(ntm * ntn), 256, 0, st>>>(p);
+  if (vec) k_gemm<V, ACT, GRP, true, OPT><<<unsigned(ntm * ntn), 256, 0, st>>>(p);
+  else k_gemm<V, ACT, GRP, false, OPT><<<unsigned(ntm * ntn), 256, 0, st>>>(p);
   return hipGetLastError();
+}
+
+// Run-time choice of the grouped-scale and zero-offset instantiations of one
+// family (OPT_BASE: 0 or kOptQ8).
+template <int V, bool ACT, int OPT_BASE>
+hipError_t launch_zg(bool grouped, bool zp, const GemmArgs& p, hipStream_t st) {
+  if (zp) return grouped ? launch_variant<V, ACT, true, OPT_BASE | kOptZ>(p, st) : launch_variant<V, ACT, false, OPT_BASE | kOptZ>(p, st);
+  return grouped ? launch_variant<V, ACT, true, OPT_BASE>(p, st) : launch_variant<V, ACT, false, OPT_BASE>(p, st);
 }
 
 }  // namespace lrqat

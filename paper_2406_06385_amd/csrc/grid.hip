@@ -14,45 +14,88 @@ namespace lrqat {
 // ============================================================================ setup
 
 // One block per (row, group): s0 = max|W0[row, group]| / (2^(b-1)-1); 0 -> 1.
+// With z0 (asymmetric): the range [min(W, 0), max(W, 0)] onto [lo, hi],
+// s0 = (max - min) / (2^b - 1), z0 = clip(lo - round(min / s0), lo, hi);
+// a zero range gives s0 = 1, z0 = 0.
 __global__ __launch_bounds__(256) void k_minmax_scale(const float* __restrict__ W0, int64_t k,
-                                                      int64_t gsize, int ngroups, float hi,
-                                                      float* __restrict__ s0) {
+                                                      int64_t gsize, int ngroups, int bits,
+                                                      float* __restrict__ s0, int32_t* __restrict__ z0) {
   const int64_t row = blockIdx.x / ngroups;
   const int grp = int(blockIdx.x % ngroups);
   const float* p = W0 + row * k + int64_t(grp) * gsize;
-  float amax = 0.f;
-  for (int64_t j = threadIdx.x; j < gsize; j += blockDim.x) amax = fmaxf(amax, fabsf(p[j]));
-  for (int off = 32; off > 0; off >>= 1) amax = fmaxf(amax, __shfl_xor(amax, off));
-  __shared__ float red[4];
-  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = amax;
+  float amax = 0.f, vmin = 0.f, vmax = 0.f;
+  for (int64_t j = threadIdx.x; j < gsize; j += blockDim.x) {
+    const float v = p[j];
+    amax = fmaxf(amax, fabsf(v));
+    vmin = fminf(vmin, v);
+    vmax = fmaxf(vmax, v);
+  }
+  for (int off = 32; off > 0; off >>= 1) {
+    amax = fmaxf(amax, __shfl_xor(amax, off));
+    vmin = fminf(vmin, __shfl_xor(vmin, off));
+    vmax = fmaxf(vmax, __shfl_xor(vmax, off));
+  }
+  __shared__ float red[3][4];
+  if ((threadIdx.x & 63) == 0) {
+    red[0][threadIdx.x >> 6] = amax;
+    red[1][threadIdx.x >> 6] = vmin;
+    red[2][threadIdx.x >> 6] = vmax;
+  }
   __syncthreads();
   if (threadIdx.x == 0) {
-    float a = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
-    s0[row * ngroups + grp] = a > 0.f ? a / hi : 1.f;
+    const int lo = -(1 << (bits - 1)), hi = (1 << (bits - 1)) - 1;
+    const int64_t at = row * ngroups + grp;
+    if (!z0) {
+      const float a = fmaxf(fmaxf(red[0][0], red[0][1]), fmaxf(red[0][2], red[0][3]));
+      s0[at] = a > 0.f ? a / float(hi) : 1.f;
+    } else {
+      const float mn = fminf(fminf(red[1][0], red[1][1]), fminf(red[1][2], red[1][3]));
+      const float mx = fmaxf(fmaxf(red[2][0], red[2][1]), fmaxf(red[2][2], red[2][3]));
+      const float range = mx - mn;
+      if (range > 0.f) {
+        const float s = range / float((1 << bits) - 1);
+        s0[at] = s;
+        z0[at] = min(max(lo - int(__builtin_rintf(mn / s)), lo), hi);
+      } else {
+        s0[at] = 1.f;
+        z0[at] = 0;
+      }
+    }
   }
 }
 
-// Phi0 = phi(W0 / s0).  Q8: one thread per element; packed: one per byte.
+// Phi0 = phi(W0 / s0 + z0).  Q8: one thread per element; packed: one per byte.
+// The zero offset is added outside the rounding: clip(round(2^f x) + 2^f z)
+// (fixed point), clip(round(x) + z) (INT-b); without z, round(2^f clip(x)).
 __global__ __launch_bounds__(256) void k_encode(const float* __restrict__ W0, const float* __restrict__ s0,
-                                                int64_t m, int64_t k, int64_t gsize, int ngroups, int bits,
-                                                int packed, void* __restrict__ phi0) {
+                                                const int32_t* __restrict__ z0, int64_t m, int64_t k,
+                                                int64_t gsize, int ngroups, int bits, int packed,
+                                                void* __restrict__ phi0) {
   const int lo = -(1 << (bits - 1)), hi = (1 << (bits - 1)) - 1;
   const int64_t per_row = packed ? k / 2 : k;
   const int64_t idx = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
   if (idx >= m * per_row) return;
   const int64_t row = idx / per_row, col = idx % per_row;
   if (!packed) {
-    const float x = W0[row * k + col] / s0[row * ngroups + col / gsize];
-    const float xc = fminf(fmaxf(x, float(lo)), float(hi));
+    const int64_t gi = row * ngroups + col / gsize;
+    const float x = W0[row * k + col] / s0[gi];
     const int f = 8 - bits;
-    static_cast<int8_t*>(phi0)[row * k + col] = int8_t(int(__builtin_rintf(xc * float(1 << f))));
+    int code;
+    if (z0) {
+      code = min(max(int(__builtin_rintf(x * float(1 << f))) + z0[gi] * (1 << f), lo * (1 << f)), hi * (1 << f));
+    } else {
+      const float xc = fminf(fmaxf(x, float(lo)), float(hi));
+      code = int(__builtin_rintf(xc * float(1 << f)));
+    }
+    static_cast<int8_t*>(phi0)[row * k + col] = int8_t(code);
   } else {
     int v[2];
     #pragma unroll
     for (int e = 0; e < 2; ++e) {
       const int64_t j = 2 * col + e;
-      const float x = W0[row * k + j] / s0[row * ngroups + j / gsize];
-      v[e] = min(max(int(__builtin_rintf(x)), lo), hi);
+      const int64_t gi = row * ngroups + j / gsize;
+      const float x = W0[row * k + j] / s0[gi];
+      v[e] = min(max(int(__builtin_rintf(x)) + (z0 ? z0[gi] : 0), lo), hi);
     }
     static_cast<uint8_t*>(phi0)[row * per_row + col] = uint8_t((v[0] & 15) | ((v[1] & 15) << 4));
   }
@@ -68,8 +111,8 @@ __global__ __launch_bounds__(256) void k_encode(const float* __restrict__ W0, co
 // block cb (0..3) are permuted: MFMA row i stands for column
 // 16 (i / 4) + 4 cb + i % 4, so lane l owns weight row l % 16 and the 16
 // consecutive columns 16 (l / 16) .. +15 of the tile.  Its Phi0 codes are one
-// 16-byte (Q8) or 8-byte (packed) load, its q nibbles one 8-byte store, and
-// its clip-mask bits one wave ballot per column.
+// 16-byte (Q8) or 8-byte (packed) load, its q nibbles one 8-byte store (16
+// bytes for grids wider than 4 bits), and its clip-mask bits one 16-bit store.
 //
 // Error bound of the float32 delta: the split drops terms below
 // 3.0001 * 2^-16 |a||b| per product; float32 accumulation of the 3r products
@@ -233,10 +276,9 @@ __device__ __forceinline__ uint32_t pack_nibble_bytes(uint32_t q0, uint32_t q1) 
 //    n + [w > 0].  That is certain unless |w| lies within tau of 0 or is at
 //    least 1 - tau; a wave with such an element redoes its tile with exact
 //    margins and float64 deltas (rare).
-template <bool PACKED, bool MASK, bool B4>
+template <bool PACKED, bool MASK, bool B4, bool Q8OUT>
 __device__ __forceinline__ void grid_finish(const GridArgs& a, const PhiRegs& P, const f32x4 (&acc)[4], float tau,
-                                            bool zero_delta, int64_t row, int64_t c16, int64_t rowblk, int64_t col0) {
-  const int lane = threadIdx.x & 63;
+                                            bool zero_delta, int64_t row, int64_t c16) {
   const int bits = B4 ? 4 : a.bits;  // B4: the common 4-bit grid, constant for the compiler
   const int lo = -(1 << (bits - 1)), hi = (1 << (bits - 1)) - 1;
   const int f = PACKED ? 0 : 8 - bits;
@@ -245,8 +287,9 @@ __device__ __forceinline__ void grid_finish(const GridArgs& a, const PhiRegs& P,
   auto n_of = [&](int idx) { return PACKED ? phi_code<true>(P, idx) : phi_code<false>(P, idx) >> f; };
 
   int ut[16];
-  uint32_t w0 = 0, w1 = 0;
-  uint64_t mbal = 0;
+  uint32_t w0 = 0, w1 = 0;    // 16 nibbles (q as int4)
+  uint32_t qb[4] = {0, 0, 0, 0};  // 16 bytes (q as int8, Q8OUT)
+  uint32_t mb = 0;            // clip-mask bits of the lane's 16 columns
   bool done = false;  // q words (and an all-ones mask) already formed by the byte-parallel path
   if (!zero_delta) {
     // the regime of the byte-parallel path: every |delta| below the distance of the non-tie
@@ -302,12 +345,17 @@ __device__ __forceinline__ void grid_finish(const GridArgs& a, const PhiRegs& P,
           q[g] = swar_grid_q8(P.w[g], incb, f, bits, clip);
         }
         if (!__builtin_amdgcn_ballot_w64(clip != 0)) {
-          w0 = pack_nibble_bytes(q[0], q[1]);
-          w1 = pack_nibble_bytes(q[2], q[3]);
+          if constexpr (Q8OUT) {
+#pragma unroll
+            for (int g = 0; g < 4; ++g) qb[g] = q[g];
+          } else {
+            w0 = pack_nibble_bytes(q[0], q[1]);
+            w1 = pack_nibble_bytes(q[2], q[3]);
+          }
           done = true;
         }
       }
-      mbal = ~uint64_t(0);
+      if (done) mb = 0xFFFFu;  // inside the regime every rounded value is on the grid
     }
   }
   if (done) {
@@ -372,46 +420,62 @@ __device__ __forceinline__ void grid_finish(const GridArgs& a, const PhiRegs& P,
     }
   }
 
-  // Clip and pack 16 nibbles (8 bytes; columns >= k are written as 0).  Mask:
-  // lane L writes the 16-row word of tile column L = 16 (L / 16) + idx,
-  // idx = L % 16, which is bits 16 (L / 16) .. +15 of the ballot of element idx.
+  // Clip and pack 16 nibbles (8 bytes) or 16 bytes (Q8OUT); columns >= k are
+  // written as 0.  Mask: bit idx of the lane's 16-bit word is [the rounded value
+  // of column c16 + idx lies on the grid].
   if (!done) {
 #pragma unroll
     for (int idx = 0; idx < 16; ++idx) {
       const int q = min(max(ut[idx], lo), hi);
-      const uint32_t nib = uint32_t(q & 15) << (4 * (idx & 7));
-      if (idx < 8) w0 |= nib;
-      else w1 |= nib;
-      if constexpr (MASK) {
-        const uint64_t bal = __builtin_amdgcn_ballot_w64(q == ut[idx]);
-        mbal = (lane & 15) == idx ? bal : mbal;
+      if constexpr (Q8OUT) {
+        qb[idx >> 2] |= uint32_t(q & 255) << (8 * (idx & 3));
+      } else {
+        const uint32_t nib = uint32_t(q & 15) << (4 * (idx & 7));
+        if (idx < 8) w0 |= nib;
+        else w1 |= nib;
       }
+      if constexpr (MASK) mb |= uint32_t(q == ut[idx]) << idx;
     }
   }
   if (kin < 16) {
-    const uint64_t keep = (uint64_t(1) << (4 * kin)) - 1;  // kin <= 15
-    w0 &= uint32_t(keep);
-    w1 &= uint32_t(keep >> 32);
-  }
-  if (row_ok && c16 < a.kq) {
-    uint8_t* dst = a.qout + row * a.ldq + (c16 >> 1);
-    if (c16 + 16 <= a.kq && (reinterpret_cast<uintptr_t>(dst) & 7) == 0) {
-      *reinterpret_cast<u32x2*>(dst) = u32x2{w0, w1};
+    if constexpr (Q8OUT) {
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int nb = kin - 4 * g;  // bytes of word g inside k
+        qb[g] &= nb >= 4 ? 0xFFFFFFFFu : nb <= 0 ? 0u : (1u << (8 * nb)) - 1u;
+      }
     } else {
-      const int64_t nbytes = min<int64_t>(8, (a.kq - c16 + 1) >> 1);
-      for (int64_t b = 0; b < nbytes; ++b) dst[b] = uint8_t((b < 4 ? w0 : w1) >> (8 * (b & 3)));
+      const uint64_t keep = (uint64_t(1) << (4 * kin)) - 1;  // kin <= 15
+      w0 &= uint32_t(keep);
+      w1 &= uint32_t(keep >> 32);
     }
   }
-  if constexpr (MASK) {
-    const int64_t col = col0 + lane;
-    if (col < a.kq) a.mout[rowblk * a.ldm + col] = uint16_t(mbal >> (16 * (lane >> 4)));
+  if (row_ok && c16 < a.kq) {
+    if constexpr (Q8OUT) {
+      uint8_t* dst = a.qout + row * a.ldq + c16;
+      if (c16 + 16 <= a.kq && (reinterpret_cast<uintptr_t>(dst) & 15) == 0) {
+        *reinterpret_cast<u32x4*>(dst) = u32x4{qb[0], qb[1], qb[2], qb[3]};
+      } else {
+        const int64_t nbytes = min<int64_t>(16, a.kq - c16);
+        for (int64_t b = 0; b < nbytes; ++b) dst[b] = uint8_t(qb[b >> 2] >> (8 * (b & 3)));
+      }
+    } else {
+      uint8_t* dst = a.qout + row * a.ldq + (c16 >> 1);
+      if (c16 + 16 <= a.kq && (reinterpret_cast<uintptr_t>(dst) & 7) == 0) {
+        *reinterpret_cast<u32x2*>(dst) = u32x2{w0, w1};
+      } else {
+        const int64_t nbytes = min<int64_t>(8, (a.kq - c16 + 1) >> 1);
+        for (int64_t b = 0; b < nbytes; ++b) dst[b] = uint8_t((b < 4 ? w0 : w1) >> (8 * (b & 3)));
+      }
+    }
+    if constexpr (MASK) a.mout[row * a.ldm + (c16 >> 4)] = uint16_t(mb);
   }
 }
 
 // COAL (r = 32, 16-byte aligned A and B rows, k % 4 == 0): B and A are read
 // with coalesced 16-byte loads and rearranged into MFMA operand order in the
 // wave's LDS region; otherwise each lane loads its own operand values.
-template <bool PACKED, bool ONEK, bool MASK, bool COAL, bool B4>
+template <bool PACKED, bool ONEK, bool MASK, bool COAL, bool B4, bool Q8OUT>
 __global__ __launch_bounds__(GR_THREADS) void k_grid(GridArgs a) {
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x >> 6));
@@ -599,50 +663,90 @@ __global__ __launch_bounds__(GR_THREADS) void k_grid(GridArgs a) {
     // -1 where delta is exactly zero (a zero A row or zero B columns, e.g. B at its zero
     // initialisation), so that no element is re-decided there
     const float tau = amx == 0.f ? -1.f : a.tau_coef * norm_bound(ass, amx, a.r) * nb;
-    grid_finish<PACKED, MASK, B4>(a, Pc, acc, tau, bmx == 0.f, row, c16, rowblk, col0);
+    grid_finish<PACKED, MASK, B4, Q8OUT>(a, Pc, acc, tau, bmx == 0.f, row, c16);
   }
 }
 
 // ============================================================================ activations
 // One block per token row: s_x = max|X_t| / 127, n = clip(round(X_t / s_x), -128, 127).
-// Columns k..ldn-1 of n are written as 0.
+// Outputs (each optional): the codes n [T][ldn] (columns k..ldn-1 written as
+// 0), X_hat = s_x n rounded to bfloat16 [T][ldh], and s_x [T].  VEC: k % 8 == 0
+// and 16-byte aligned rows, read and written as 16-byte vectors.
+template <bool VEC>
 __global__ __launch_bounds__(256) void k_act_quant(const uint16_t* __restrict__ X, int64_t k,
                                                    int8_t* __restrict__ n, int64_t ldn,
+                                                   uint16_t* __restrict__ xh, int64_t ldh,
                                                    float* __restrict__ sx) {
   const int64_t row = blockIdx.x;
   const uint16_t* x = X + row * k;
   float amax = 0.f;
-  for (int64_t j = threadIdx.x; j < k; j += 256) amax = fmaxf(amax, fabsf(bf16_to_f32(x[j])));
+  if (VEC) {
+    for (int64_t j = 8 * threadIdx.x; j < k; j += 8 * 256) {
+      const u32x4 v = *reinterpret_cast<const u32x4*>(x + j);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) amax = fmaxf(amax, fmaxf(fabsf(bf16_lo(v[q])), fabsf(bf16_hi(v[q]))));
+    }
+  } else {
+    for (int64_t j = threadIdx.x; j < k; j += 256) amax = fmaxf(amax, fabsf(bf16_to_f32(x[j])));
+  }
   for (int off = 32; off > 0; off >>= 1) amax = fmaxf(amax, __shfl_xor(amax, off));
   __shared__ float red[4];
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = amax;
   __syncthreads();
   amax = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
   const float s = amax / 127.f;
-  if (threadIdx.x == 0) sx[row] = s;
-  int8_t* out = n + row * ldn;
-  for (int64_t j = threadIdx.x; j < ldn; j += 256) {
-    int v = 0;
-    if (j < k && s > 0.f) v = min(max(int(__builtin_rintf(bf16_to_f32(x[j]) / s)), -128), 127);
-    out[j] = int8_t(v);
+  if (threadIdx.x == 0 && sx) sx[row] = s;
+  auto code = [&](float v) { return s > 0.f ? min(max(int(__builtin_rintf(v / s)), -128), 127) : 0; };
+  if (VEC) {
+    for (int64_t j = 8 * threadIdx.x; j < k; j += 8 * 256) {
+      const u32x4 v = *reinterpret_cast<const u32x4*>(x + j);
+      int c[8];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        c[2 * q] = code(bf16_lo(v[q]));
+        c[2 * q + 1] = code(bf16_hi(v[q]));
+      }
+      if (n) {
+        u32x2 o;
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+          o[h] = uint32_t(c[4 * h] & 255) | (uint32_t(c[4 * h + 1] & 255) << 8) | (uint32_t(c[4 * h + 2] & 255) << 16) |
+                 (uint32_t(c[4 * h + 3] & 255) << 24);
+        *reinterpret_cast<u32x2*>(n + row * ldn + j) = o;
+      }
+      if (xh) {
+        u32x4 o;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) o[q] = pack_bf16x2(float(c[2 * q]) * s, float(c[2 * q + 1]) * s);
+        *reinterpret_cast<u32x4*>(xh + row * ldh + j) = o;
+      }
+    }
+    if (n)
+      for (int64_t j = k + threadIdx.x; j < ldn; j += 256) n[row * ldn + j] = 0;
+  } else {
+    const int64_t end = n ? ldn : k;
+    for (int64_t j = threadIdx.x; j < end; j += 256) {
+      const int c = j < k ? code(bf16_to_f32(x[j])) : 0;
+      if (n) n[row * ldn + j] = int8_t(c);
+      if (xh && j < k) xh[row * ldh + j] = __builtin_bit_cast(uint16_t, (__bf16)(float(c) * s));
+    }
   }
 }
 
 // ============================================================================ launchers
 
-hipError_t launch_minmax_scale(const float* W0, int64_t m, int64_t k, int64_t gsize, int bits, float* s0,
+hipError_t launch_minmax_scale(const float* W0, int64_t m, int64_t k, int64_t gsize, int bits, float* s0, int32_t* z0,
                                hipStream_t st) {
   const int ngroups = int(k / gsize);
-  k_minmax_scale<<<unsigned(m * ngroups), 256, 0, st>>>(W0, k, gsize, ngroups,
-                                                          float((1 << (bits - 1)) - 1), s0);
+  k_minmax_scale<<<unsigned(m * ngroups), 256, 0, st>>>(W0, k, gsize, ngroups, bits, s0, z0);
   return hipGetLastError();
 }
 
-hipError_t launch_encode(const float* W0, const float* s0, int64_t m, int64_t k, int64_t gsize, int bits,
-                         int packed, void* phi0, hipStream_t st) {
+hipError_t launch_encode(const float* W0, const float* s0, const int32_t* z0, int64_t m, int64_t k, int64_t gsize,
+                         int bits, int packed, void* phi0, hipStream_t st) {
   const int64_t n = m * (packed ? k / 2 : k);
   const int ngroups = int(k / gsize);
-  k_encode<<<unsigned((n + 255) / 256), 256, 0, st>>>(W0, s0, m, k, gsize, ngroups, bits, packed, phi0);
+  k_encode<<<unsigned((n + 255) / 256), 256, 0, st>>>(W0, s0, z0, m, k, gsize, ngroups, bits, packed, phi0);
   return hipGetLastError();
 }
 
@@ -660,11 +764,30 @@ hipError_t launch_grid(const GridArgs& a0, hipStream_t st) {
   // 4-bit grids (the common W4 case) get an instantiation with the width fixed
   const int sel = (a.packed ? 8 : 0) | (a.r <= 32 ? 4 : 0) | (coal ? 2 : 0) | (a.mout ? 1 : 0);
   const bool b4 = a.bits == 4;
+  // grids wider than 4 bits (fixed point b = 5..7) are written as int8
+  if (a.q8out) {
+    if (a.packed || a.bits <= 4) return hipErrorInvalidValue;
+    switch (sel) {
+#define LRQAT_GRID8_CASE(S, O, C, M)                                        \
+  case S:                                                                   \
+    k_grid<false, O, M, C, false, true><<<nb, GR_THREADS, 0, st>>>(a);      \
+    break;
+      LRQAT_GRID8_CASE(0, false, false, false)
+      LRQAT_GRID8_CASE(1, false, false, true)
+      LRQAT_GRID8_CASE(4, true, false, false)
+      LRQAT_GRID8_CASE(5, true, false, true)
+      LRQAT_GRID8_CASE(6, true, true, false)
+      LRQAT_GRID8_CASE(7, true, true, true)
+#undef LRQAT_GRID8_CASE
+      default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+  }
   switch (sel) {
 #define LRQAT_GRID_CASE(S, P, O, C, M)                                      \
   case S:                                                                   \
-    if (b4) k_grid<P, O, M, C, true><<<nb, GR_THREADS, 0, st>>>(a);         \
-    else k_grid<P, O, M, C, false><<<nb, GR_THREADS, 0, st>>>(a);           \
+    if (b4) k_grid<P, O, M, C, true, false><<<nb, GR_THREADS, 0, st>>>(a);  \
+    else k_grid<P, O, M, C, false, false><<<nb, GR_THREADS, 0, st>>>(a);    \
     break;
     LRQAT_GRID_CASE(0, false, false, false, false)
     LRQAT_GRID_CASE(1, false, false, false, true)
@@ -684,9 +807,14 @@ hipError_t launch_grid(const GridArgs& a0, hipStream_t st) {
   return hipGetLastError();
 }
 
-hipError_t launch_act_quant(const uint16_t* X, int64_t T, int64_t k, int8_t* n, int64_t ldn, float* sx,
-                            hipStream_t st) {
-  k_act_quant<<<unsigned(T), 256, 0, st>>>(X, k, n, ldn, sx);
+hipError_t launch_act_quant(const uint16_t* X, int64_t T, int64_t k, int8_t* n, int64_t ldn, uint16_t* xh, int64_t ldh,
+                            float* sx, hipStream_t st) {
+  if (T == 0) return hipSuccess;
+  const bool vec = k % 8 == 0 && (reinterpret_cast<uintptr_t>(X) & 15) == 0 && (!n || ldn % 8 == 0) &&
+                   (!xh || (ldh % 8 == 0 && (reinterpret_cast<uintptr_t>(xh) & 15) == 0)) &&
+                   (reinterpret_cast<uintptr_t>(n) & 7) == 0;
+  if (vec) k_act_quant<true><<<unsigned(T), 256, 0, st>>>(X, k, n, ldn, xh, ldh, sx);
+  else k_act_quant<false><<<unsigned(T), 256, 0, st>>>(X, k, n, ldn, xh, ldh, sx);
   return hipGetLastError();
 }
 

@@ -11,8 +11,9 @@ namespace lrqat {
 // and cf the f fraction bits, round-half-even(n + cf 2^-f + delta) is n plus
 // the carry out of cf + (2^(f-1) - 1) + [delta > 0], since only a tie
 // (cf = 2^(f-1)) depends on delta.  incb holds [delta > 0] per byte.  Returns
-// the 4-bit two's-complement codes in the low nibble of each byte; clip marks
-// (bit 7 of a byte) the codes that would leave the grid (n = hi with a carry).
+// the codes as two's complement, in the low nibble of each byte for b <= 4 and
+// as whole signed bytes for b >= 5; clip marks (bit 7 of a byte) the codes
+// that would leave the grid (n = hi with a carry).
 __host__ __device__ __forceinline__ uint32_t swar_grid_q8(uint32_t w, uint32_t incb, int f, int b, uint32_t& clip) {
   const uint32_t ones = 0x01010101u;
   const uint32_t t = (w & (ones * ((1u << f) - 1))) + ones * ((1u << (f - 1)) - 1) + incb;
@@ -22,7 +23,8 @@ __host__ __device__ __forceinline__ uint32_t swar_grid_q8(uint32_t w, uint32_t i
   const uint32_t e = nu ^ (ones * ((1u << (b - 1)) - 1));   // zero where n = hi
   clip |= ~(((e + 0x7F7F7F7Fu) | e) & 0x80808080u) & (carry << 7);
   uint32_t qu = (nu + carry) & mn;
-  if (b < 4) qu |= (qu & (ones << (b - 1))) * ((16u - (1u << b)) >> (b - 1));  // sign-extend to 4 bits
+  if (b < 4) qu |= (qu & (ones << (b - 1))) * ((16u - (1u << b)) >> (b - 1));        // sign-extend to 4 bits
+  else if (b > 4) qu |= (qu & (ones << (b - 1))) * ((256u - (1u << b)) >> (b - 1));  // to 8 bits
   return qu;
 }
 

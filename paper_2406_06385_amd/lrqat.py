@@ -83,7 +83,10 @@ def _lib():
         lib.lrqat_forward_workspace_size.restype = SZ
         lib.lrqat_backward_workspace_size.argtypes = [F, I64]
         lib.lrqat_backward_workspace_size.restype = SZ
-        lib.lrqat_init_from_weights.argtypes = [F, P, P, P, P]
+        lib.lrqat_init_from_weights.argtypes = [F, P, P, P, P, P]
+        lib.lrqat_infer_workspace_size.argtypes = [F, I64]
+        lib.lrqat_infer_workspace_size.restype = SZ
+        lib.lrqat_infer_forward.argtypes = [F, I64, P, P, P, P, P, P, SZ, P]
         lib.lrqat_forward.argtypes = [F, I64, P, P, P, P, P, P, P, P, SZ, P]
         lib.lrqat_backward.argtypes = [F, I64, P, P, P, P, P, P, P, P, P, P, P, ctypes.c_int, P, SZ, P]
         lib.lrqat_backward_static.argtypes = [F, I64, P, P, P, P, P, P, P, P, P, P, P, ctypes.c_int, P]
@@ -91,7 +94,7 @@ def _lib():
         lib.lrqat_backward_static_capacity.restype = SZ
         lib.lrqat_merge_to_int4.argtypes = [F, P, P, P, P, P]
         for fn in ("lrqat_init_from_weights", "lrqat_forward", "lrqat_backward", "lrqat_backward_static",
-                   "lrqat_merge_to_int4"):
+                   "lrqat_merge_to_int4", "lrqat_infer_forward"):
             getattr(lib, fn).restype = ctypes.c_int
         lib.lrqat_status_string.argtypes = [ctypes.c_int]
         lib.lrqat_status_string.restype = ctypes.c_char_p
@@ -177,16 +180,18 @@ def workspace(nbytes: int, device="cuda") -> torch.Tensor:
     return torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=device)
 
 
-def lrqat_init_from_weights(spec: LayerSpec, W0: torch.Tensor, stream=None):
-    """-> (s0 float32, Phi0) computed on the GPU from W0 [m][k] float32."""
+def lrqat_init_from_weights(spec: LayerSpec, W0: torch.Tensor, stream=None, asymmetric=False):
+    """-> (s0 float32, Phi0) computed on the GPU from W0 [m][k] float32, or
+    (s0, z0 int32, Phi0) with asymmetric=True (Phi0 then carries z0)."""
     _expect(W0, (spec.out_features, spec.in_features), torch.float32, "W0")
     st = _torch_stream(stream)
     with torch.cuda.stream(st):
         s0 = torch.empty(spec.scale_shape(), dtype=torch.float32, device=W0.device)
+        z0 = torch.empty(spec.scale_shape(), dtype=torch.int32, device=W0.device) if asymmetric else None
         phi0 = torch.empty(spec.phi_shape(), dtype=spec.phi_dtype, device=W0.device)
     L = spec.c_struct()
-    _check(_lib().lrqat_init_from_weights(ctypes.byref(L), _ptr(W0), _ptr(s0), _ptr(phi0), _stream(st)))
-    return s0, phi0
+    _check(_lib().lrqat_init_from_weights(ctypes.byref(L), _ptr(W0), _ptr(s0), _ptr(z0), _ptr(phi0), _stream(st)))
+    return (s0, z0, phi0) if asymmetric else (s0, phi0)
 
 
 def lrqat_forward(spec: LayerSpec, X, phi0, s, A, B, Y=None, ws=None, stream=None, z=None):
@@ -285,6 +290,38 @@ def lrqat_merge_to_int4(spec: LayerSpec, phi0, A, B, out=None, stream=None):
     L = spec.c_struct()
     _check(_lib().lrqat_merge_to_int4(ctypes.byref(L), _ptr(phi0), _ptr(A), _ptr(B), _ptr(out), _stream(st)))
     return out
+
+
+def lrqat_infer_workspace_size(spec: LayerSpec, tokens: int) -> int:
+    L = spec.c_struct()
+    n = _lib().lrqat_infer_workspace_size(ctypes.byref(L), tokens)
+    if n == 0:
+        raise LRQATError(LRQAT_EINVAL, _lib().lrqat_last_error().decode())
+    return n
+
+
+def lrqat_infer_forward(spec: LayerSpec, X, W_int4, s, z=None, Y=None, ws=None, stream=None):
+    """Y = X_hat (s (W_Z - z))^T on the merged packed int4 weights uint8 [m][k/2]."""
+    T = X.shape[0] if X.dim() == 2 else -1
+    m, k = spec.out_features, spec.in_features
+    _expect(X, (T, k), spec.torch_dtype, "X")
+    dev = X.device
+    _expect(W_int4, (m, k // 2), torch.uint8, "W_int4", dev)
+    _expect(s, spec.scale_shape(), torch.float32, "s", dev)
+    if z is not None:
+        _expect(z, spec.scale_shape(), torch.int32, "z", dev)
+    st = _torch_stream(stream)
+    with torch.cuda.stream(st):
+        if Y is None:
+            Y = torch.empty((T, m), dtype=spec.torch_dtype, device=dev)
+        if ws is None:
+            ws = workspace(lrqat_infer_workspace_size(spec, T), dev)
+    _expect(Y, (T, m), spec.torch_dtype, "Y", dev)
+    _expect(ws, (ws.numel(),), torch.uint8, "ws", dev)
+    L = spec.c_struct()
+    _check(_lib().lrqat_infer_forward(ctypes.byref(L), T, _ptr(X), _ptr(W_int4), _ptr(s), _ptr(z), _ptr(Y),
+                                      _ptr(ws), ws.numel(), _stream(st)))
+    return Y
 
 
 def lrqat_timing_enable(on: bool = True):

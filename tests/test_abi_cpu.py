@@ -69,7 +69,8 @@ def _bwd_static(lib, L, T=16):
 @pytest.mark.parametrize("kw,status", [
     (dict(bits=8), lrqat.LRQAT_EINVAL),
     (dict(bits=1), lrqat.LRQAT_EINVAL),
-    (dict(bits=5), lrqat.LRQAT_EUNSUPPORTED),
+    (dict(bits=5), lrqat.LRQAT_OK),
+    (dict(bits=7), lrqat.LRQAT_OK),
     (dict(bits=5, phi_format="int_packed2"), lrqat.LRQAT_EINVAL),
     (dict(in_features=127, phi_format="int_packed2"), lrqat.LRQAT_EINVAL),
     (dict(group_size=48), lrqat.LRQAT_EINVAL),
@@ -103,7 +104,8 @@ def test_pointer_and_workspace_errors(lib):
     assert _fwd(lib, L, ws_bytes=need - 1) == lrqat.LRQAT_EWORKSPACE
     assert _fwd(lib, L, T=-1) == lrqat.LRQAT_EINVAL
     assert _fwd(lib, L, T=0) == lrqat.LRQAT_OK          # no-op, launches nothing
-    assert _bwd(lib, L, ds=FAKE) == lrqat.LRQAT_EUNSUPPORTED
+    assert _bwd(lib, L, ds=BAD_ALIGN) == lrqat.LRQAT_EINVAL
+    assert _fwd(lib, L, z=BAD_ALIGN) == lrqat.LRQAT_EINVAL
     assert _bwd(lib, L, accumulate=2) == lrqat.LRQAT_EINVAL
     assert _bwd(lib, L, dX=BAD_ALIGN) == lrqat.LRQAT_EINVAL
     needb = lib.lrqat_backward_workspace_size(ctypes.byref(L), 16)
@@ -112,7 +114,18 @@ def test_pointer_and_workspace_errors(lib):
     assert lib.lrqat_merge_to_int4(ctypes.byref(_layer(in_features=127)), P(FAKE), P(FAKE), P(FAKE), P(FAKE),
                                    None) == lrqat.LRQAT_EINVAL
     assert lib.lrqat_merge_to_int4(ctypes.byref(L), P(FAKE), P(FAKE), P(FAKE), P(0), None) == lrqat.LRQAT_EINVAL
-    assert lib.lrqat_init_from_weights(ctypes.byref(L), P(0), P(FAKE), P(FAKE), None) == lrqat.LRQAT_EINVAL
+    assert lib.lrqat_init_from_weights(ctypes.byref(L), P(0), P(FAKE), None, P(FAKE), None) == lrqat.LRQAT_EINVAL
+    assert lib.lrqat_init_from_weights(ctypes.byref(L), P(FAKE), P(FAKE), P(BAD_ALIGN), P(FAKE),
+                                       None) == lrqat.LRQAT_EINVAL
+    # inference on merged weights: int4 only, argument checks before any launch
+    assert lib.lrqat_infer_forward(ctypes.byref(_layer(bits=5)), 16, P(FAKE), P(FAKE), P(FAKE), None, P(FAKE),
+                                   P(FAKE), 1 << 30, None) == lrqat.LRQAT_EINVAL
+    assert lib.lrqat_infer_forward(ctypes.byref(L), 16, P(0), P(FAKE), P(FAKE), None, P(FAKE), P(FAKE), 1 << 30,
+                                   None) == lrqat.LRQAT_EINVAL
+    La = _layer(act_bits=8)  # W4A8 needs workspace for the activation codes
+    assert lib.lrqat_infer_forward(ctypes.byref(La), 16, P(FAKE), P(FAKE), P(FAKE), None, P(FAKE), P(FAKE), 0,
+                                   None) == lrqat.LRQAT_EWORKSPACE
+    assert lib.lrqat_infer_workspace_size(ctypes.byref(L), 16) >= 256
     assert lib.lrqat_forward(None, 16, P(FAKE), P(FAKE), P(FAKE), None, P(FAKE), P(FAKE), P(FAKE), P(FAKE),
                              1 << 30, None) == lrqat.LRQAT_EINVAL
 

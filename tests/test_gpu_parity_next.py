@@ -1,0 +1,235 @@
+"""GPU parity of the rows after the hot path (marked gpu): the asymmetric zero
+offset and the scale gradient ds, fixed-point grids of 5..7 bits, and inference
+on the merged int4 weights, each against the CPU oracle on seeded inputs.
+
+Criteria as in test_gpu_parity: setup outputs (s0, z0, Phi0) and merge bytes
+bit-exact; Y, dX, dA, dB, ds within 1e-4 (float32 activations) or 2e-2
+(bfloat16) relative, by Frobenius norm and per row and column (lines whose
+own ratio is larger must stay below 2^-6 of the magnitude of their terms).
+The grid of 5..7-bit layers is checked exactly through the float32 path with
+an identity input (Y = X W_hat^T = W_hat)."""
+import sys
+
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+from oracle import lrqat_oracle as O
+from paper_2406_06385_amd import inputs as I
+from test_gpu_parity import TOL, act_values, assert_close, errors, from_dev, to_dev_act
+
+pytestmark = pytest.mark.gpu
+
+
+def _log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+@pytest.fixture(scope="module")
+def lr():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2406_06385_amd import lrqat
+    lrqat.load_library()
+    return lrqat
+
+
+class Layer:
+    """Seeded layer with both sides' setup; asym=True uses the zero offset."""
+
+    def __init__(self, lr, m, k, T, r, alpha, bits, fmt, g=0, act=0, dtype="bf16", asym=False, seed=3,
+                 b_std=1e-3, a_scale=1.0, shift=0.0):
+        self.spec = lr.LayerSpec(m, k, r, alpha, bits, fmt, g, act, dtype)
+        self.L = O.Layer(m, k, r, alpha, bits, fmt, g, act)
+        self.dtype, self.T, self.asym = dtype, T, asym
+        self.W0 = (I.gen_w0(m, k, seed, seed + 1, 0.02, 0.0) + np.float32(shift)).astype(np.float32)
+        self.A = (I.gen_a(m, r, k, seed + 2) * np.float32(a_scale)).astype(np.float32)
+        self.B = I.gen_b(r, k, seed + 3, b_std)
+        self.X = I.gen_act(T, k, seed + 4, 1.0, dtype)
+        self.dY = I.gen_act(T, m, seed + 5, 1e-2, dtype)
+        d_W0 = torch.from_numpy(self.W0).cuda()
+        if asym:
+            self.s_ref, self.z_ref = O.minmax_scale_zero(self.W0, bits, g)
+            self.d_s, self.d_z, self.d_phi = lr.lrqat_init_from_weights(self.spec, d_W0, asymmetric=True)
+        else:
+            self.s_ref, self.z_ref = O.minmax_scale(self.W0, bits, g), None
+            self.d_s, self.d_phi = lr.lrqat_init_from_weights(self.spec, d_W0)
+            self.d_z = None
+        self.phi_ref = O.encode_phi0(self.W0, self.s_ref, bits, fmt, g, self.z_ref)
+        self.d_A = torch.from_numpy(self.A).cuda()
+        self.d_B = torch.from_numpy(self.B).cuda()
+        self.d_X = to_dev_act(self.X, dtype)
+        self.d_dY = to_dev_act(self.dY, dtype)
+        self.Xv = act_values(self.X, dtype)
+        self.dYv = act_values(self.dY, dtype).astype(np.float64)
+
+    def check_setup(self):
+        assert np.array_equal(self.d_s.cpu().numpy().reshape(self.s_ref.shape), self.s_ref), "s0 differs"
+        if self.asym:
+            assert np.array_equal(self.d_z.cpu().numpy().reshape(self.z_ref.shape), self.z_ref), "z0 differs"
+        assert np.array_equal(self.d_phi.cpu().numpy(), self.phi_ref), "Phi0 differs"
+
+
+def check_layer(lr, c, want_ds=True):
+    L = c.L
+    Y = lr.lrqat_forward(c.spec, c.d_X, c.d_phi, c.d_s, c.d_A, c.d_B, z=c.d_z)
+    out = lr.lrqat_backward(c.spec, c.d_X, c.d_phi, c.d_s, c.d_A, c.d_B, c.d_dY, z=c.d_z, want_ds=want_ds)
+    torch.cuda.synchronize()
+    Y, dX = from_dev(Y), from_dev(out[0])
+    dA, dB = out[1].cpu().numpy(), out[2].cpu().numpy()
+    z = c.z_ref
+    Yr = O.forward(L, c.Xv, c.phi_ref, c.s_ref, c.A, c.B, z)[0]
+    gr = O.backward(L, c.Xv, c.phi_ref, c.s_ref, c.A, c.B, c.dYv, z)
+    tol = TOL[c.dtype]
+    allt, allr, allc = np.arange(c.T), np.arange(L.m), np.arange(L.k)
+    errs = {
+        "Y": errors(Y, Yr, O.forward_rows_abs(L, c.Xv, c.phi_ref, c.s_ref, c.A, c.B, allt, z), tol),
+        "dX": errors(dX, gr["dX"], O.dx_rows_abs(L, c.phi_ref, c.s_ref, c.A, c.B, c.dYv, allt, z), tol),
+        "dA": errors(dA, gr["dA"], O.da_rows_abs(L, c.Xv, c.phi_ref, c.s_ref, c.A, c.B, c.dYv, allr), tol),
+        "dB": errors(dB, gr["dB"], O.db_cols_abs(L, c.Xv, c.phi_ref, c.s_ref, c.A, c.B, c.dYv, allc), tol),
+    }
+    if want_ds:
+        ds = out[3].cpu().numpy().reshape(gr["ds"].shape)
+        mag = O.ds_rows_abs(L, c.Xv, c.phi_ref, c.s_ref, c.A, c.B, c.dYv, allr, z)
+        errs["ds"] = errors(ds.reshape(L.m, -1), gr["ds"].reshape(L.m, -1), mag.reshape(L.m, -1), tol)
+    _log(f"  errors (fro, row, col) {errs}")
+    assert_close(errs, tol)
+    return errs
+
+
+# ----------------------------------------------------------------------------- zero offset and ds
+
+ASYM = [
+    # m, k, T, r, alpha, bits, fmt, g, act, dtype
+    (320, 264, 96, 16, 16.0, 2, "q8", 0, 0, "bf16"),           # W2 asymmetric, Q2.6, ragged
+    (256, 512, 128, 8, 8.0, 2, "int_packed2", 128, 0, "bf16"),  # W2 asymmetric INT2 g128
+    (300, 256, 77, 8, 8.0, 3, "q8", 64, 0, "bf16"),            # W3 g64
+    (512, 256, 128, 8, 8.0, 2, "q8", 0, 0, "fp32"),            # float32 path
+    (384, 640, 200, 32, 32.0, 4, "int_packed2", 0, 8, "bf16"),  # with W4A8
+]
+
+
+@pytest.mark.parametrize("shape", ASYM, ids=[f"m{s[0]}k{s[1]}b{s[5]}{s[6]}g{s[7]}a{s[8]}{s[9]}" for s in ASYM])
+def test_asymmetric_zero_offset_with_scale_gradient(lr, shape):
+    m, k, T, r, alpha, bits, fmt, g, act, dtype = shape
+    _log(f"[asymmetric {shape}]")
+    c = Layer(lr, m, k, T, r, alpha, bits, fmt, g, act, dtype, asym=True, seed=40 + m, shift=0.01, b_std=0.05)
+    assert (c.z_ref != 0).any()
+    c.check_setup()
+    W = lr.lrqat_merge_to_int4(c.spec, c.d_phi, c.d_A, c.d_B).cpu().numpy()
+    q_ref, _, near, _ = O.grid_from_inputs(c.phi_ref, c.A, c.B, alpha, r, bits, fmt)
+    bad = O.unpack_int4(W) != q_ref
+    assert not (bad & ~near).any()
+    check_layer(lr, c)
+
+
+SYM_DS = [
+    (4096, 4096, 512, 32, 32.0, 4, "q8", 0, 0, "bf16"),     # the 4096 x 4096 layer, fewer tokens
+    (520, 768, 300, 64, 64.0, 3, "q8", 128, 0, "bf16"),     # W3 g128, ragged m and T
+    (384, 640, 96, 32, 32.0, 4, "int_packed2", 0, 0, "bf16"),
+    (300, 264, 77, 8, 8.0, 4, "q8", 0, 0, "fp32"),
+]
+
+
+@pytest.mark.parametrize("shape", SYM_DS, ids=[f"m{s[0]}k{s[1]}b{s[5]}{s[6]}g{s[7]}{s[9]}" for s in SYM_DS])
+def test_scale_gradient_symmetric(lr, shape):
+    m, k, T, r, alpha, bits, fmt, g, act, dtype = shape
+    _log(f"[ds {shape}]")
+    c = Layer(lr, m, k, T, r, alpha, bits, fmt, g, act, dtype, seed=60 + m)
+    c.check_setup()
+    check_layer(lr, c)
+
+
+def test_scale_gradient_accumulates_and_is_deterministic(lr):
+    c = Layer(lr, 512, 512, 128, 16, 16.0, 4, "q8", 128, 0, "bf16", seed=5)
+    kw = dict(want_ds=True)
+    a = lr.lrqat_backward(c.spec, c.d_X, c.d_phi, c.d_s, c.d_A, c.d_B, c.d_dY, **kw)
+    b = lr.lrqat_backward(c.spec, c.d_X, c.d_phi, c.d_s, c.d_A, c.d_B, c.d_dY, **kw)
+    ds0 = torch.full_like(a[3], 0.75)
+    acc = lr.lrqat_backward(c.spec, c.d_X, c.d_phi, c.d_s, c.d_A, c.d_B, c.d_dY, ds=ds0.clone(), accumulate=True)
+    torch.cuda.synchronize()
+    assert torch.equal(a[3], b[3])
+    assert torch.allclose(acc[3], a[3] + 0.75, rtol=1e-6, atol=1e-6)
+
+
+# ----------------------------------------------------------------------------- grids of 5..7 bits
+
+WIDE = [
+    (256, 512, 128, 32, 32.0, 5, "q8", 0, 0, "bf16"),
+    (320, 264, 96, 16, 16.0, 6, "q8", 0, 0, "bf16"),
+    (300, 512, 77, 8, 8.0, 7, "q8", 64, 0, "bf16"),
+    (384, 640, 200, 32, 32.0, 6, "q8", 0, 8, "bf16"),
+    (256, 256, 64, 8, 8.0, 7, "q8", 0, 0, "fp32"),
+]
+
+
+@pytest.mark.parametrize("shape", WIDE, ids=[f"m{s[0]}k{s[1]}b{s[5]}g{s[7]}a{s[8]}{s[9]}" for s in WIDE])
+def test_wide_fixed_point_grids(lr, shape):
+    m, k, T, r, alpha, bits, fmt, g, act, dtype = shape
+    _log(f"[wide grid {shape}]")
+    # B std 0.05 with alpha = r flips many roundings of the 5..7-bit grid
+    c = Layer(lr, m, k, T, r, alpha, bits, fmt, g, act, dtype, seed=80 + bits, b_std=0.05)
+    c.check_setup()
+    check_layer(lr, c)
+
+
+@pytest.mark.parametrize("bits,asym", [(5, False), (6, True), (7, False), (4, True), (3, False)])
+def test_grid_exact_through_identity(lr, bits, asym):
+    """The float32 forward of X = I_k gives Y = W_hat^T (one nonzero term per
+    output, s (q - z) rounded once to float32), so round(Y / s) + z is the
+    device's grid: it must equal the oracle's except inside the .5 window."""
+    m, k, r = 200, 264, 16
+    spec_b = (m, k, k, r, float(r), bits, "q8", 0, 0, "fp32")
+    c = Layer(lr, *spec_b, asym=asym, seed=90 + bits, b_std=0.05, a_scale=3.0, shift=0.01 if asym else 0.0)
+    c.check_setup()
+    X = torch.eye(k, dtype=torch.float32, device="cuda")
+    Y = lr.lrqat_forward(c.spec, X, c.d_phi, c.d_s, c.d_A, c.d_B, z=c.d_z)
+    torch.cuda.synchronize()
+    Wt = Y.cpu().numpy().astype(np.float64).T  # [m][k] = fl32(s (q - z))
+    s = c.s_ref.astype(np.float64)[:, None]
+    qz = Wt / s
+    assert np.all(np.abs(qz - np.rint(qz)) <= 2.0 ** -20 * np.abs(qz)), "the identity forward gives s times integers"
+    q_dev = np.rint(qz).astype(np.int64) + (0 if c.z_ref is None else c.z_ref[:, None])
+    q_ref, _, near, _ = O.grid_from_inputs(c.phi_ref, c.A, c.B, float(r), r, bits, "q8")
+    bad = q_dev != q_ref
+    _log(f"  {int(bad.sum())} mismatches, {int(near.sum())} near .5")
+    assert not (bad & ~near).any()
+    assert bad.sum() < 1e-4 * bad.size + 1
+    lo, hi = O.grid_limits(bits)
+    assert q_dev.min() >= lo and q_dev.max() <= hi
+    assert (q_ref != np.rint(O.decode_phi0(c.phi_ref, bits, "q8"))).sum() > 100  # the adapters moved the grid
+
+
+# ----------------------------------------------------------------------------- inference on merged weights
+
+INFER = [
+    # m, k, T, bits, fmt, g, act, asym
+    (4096, 4096, 1024, 4, "q8", 0, 0, False),
+    (384, 640, 333, 4, "int_packed2", 0, 8, False),   # W4A8
+    (520, 768, 300, 3, "q8", 128, 0, False),          # W3 g128
+    (320, 264, 96, 2, "q8", 0, 0, True),              # W2 asymmetric, k not a multiple of 32
+    (256, 512, 64, 4, "int_packed2", 0, 0, False),
+]
+
+
+@pytest.mark.parametrize("case", INFER, ids=[f"m{s[0]}k{s[1]}T{s[2]}b{s[3]}g{s[5]}a{s[6]}{'z' if s[7] else ''}" for s in INFER])
+def test_inference_on_merged_weights(lr, case):
+    m, k, T, bits, fmt, g, act, asym = case
+    _log(f"[inference {case}]")
+    c = Layer(lr, m, k, T, 32, 32.0, bits, fmt, g, act, "bf16", asym=asym, seed=120 + m, b_std=0.05,
+              shift=0.01 if asym else 0.0)
+    Wz = lr.lrqat_merge_to_int4(c.spec, c.d_phi, c.d_A, c.d_B)
+    Y = lr.lrqat_infer_forward(c.spec, c.d_X, Wz, c.d_s, z=c.d_z)
+    Yt = lr.lrqat_forward(c.spec, c.d_X, c.d_phi, c.d_s, c.d_A, c.d_B, z=c.d_z)
+    torch.cuda.synchronize()
+    Wz_ref = O.merge_to_int4(c.L, c.phi_ref, c.A, c.B)
+    assert np.array_equal(Wz.cpu().numpy(), Wz_ref), "merged bytes differ"
+    Yr = O.infer_forward(c.L, c.Xv, Wz_ref, c.s_ref, c.z_ref)
+    tol = TOL["bf16"]
+    mag = np.abs(O.layer_input(c.Xv, act)) @ np.abs(O.weight_hat(O.unpack_int4(Wz_ref), c.s_ref, g, c.z_ref)).T
+    errs = {"Y": errors(from_dev(Y), Yr, mag, tol)}
+    _log(f"  errors (fro, row, col) {errs}")
+    assert_close(errs, tol)
+    # the training-time forward of the same layer gives the same bits (same GEMM, same grid)
+    assert torch.equal(Y.view(torch.int16), Yt.view(torch.int16))

@@ -90,11 +90,12 @@ def swar_driver(tmp_path_factory):
 
 def test_byte_parallel_grid_matches_exact_rounding(swar_driver):
     """Four Q8 codes per word, delta of a known sign and magnitude below 2^-f:
-    each byte's nibble equals round-half-even(code 2^-f + delta) on the grid,
+    each byte's nibble (b <= 4) or whole byte (b >= 5) equals
+    round-half-even(code 2^-f + delta) on the grid,
     and exactly the codes that would leave the grid are marked for clipping."""
     rng = np.random.default_rng(7)
     cases = []
-    for b in (4, 3, 2):
+    for b in (7, 6, 5, 4, 3, 2):
         f = 8 - b
         for code in range(-128, 128):  # every code, in every byte position, both delta signs
             for pos in range(4):
@@ -127,6 +128,6 @@ def test_byte_parallel_grid_matches_exact_rounding(swar_driver):
             got_clip = (clip >> (8 * j + 7)) & 1
             if got_clip != int(clipped):
                 bad.append(("clip", code, f, int(incs[j]), want, got_clip))
-            elif not clipped and ((q >> (8 * j)) & 0xFF) != (want & 15):
+            elif not clipped and ((q >> (8 * j)) & 0xFF) != (want & (0xFF if b > 4 else 15)):
                 bad.append(("q", code, f, int(incs[j]), want, (q >> (8 * j)) & 0xFF))
     assert not bad, bad[:10]
