@@ -205,6 +205,46 @@ lrqat_status lrqat_infer_forward(const lrqat_layer* layer, int64_t tokens, const
                                  const uint8_t* W_int4, const float* s, const int32_t* z, void* Y,
                                  void* ws, size_t ws_bytes, void* stream);
 
+/*
+ * Optimizer step for the trainable tensors (Appendix B, Table B1): AdamW with
+ * decoupled weight decay (p <- p (1 - lr wd); m <- b1 m + (1 - b1) g;
+ * v <- b2 v + (1 - b2) g^2; p <- p - lr (m / (1 - b1^t)) / (sqrt(v / (1 - b2^t)) + eps)),
+ * on gradients clipped together to an L2 norm of at most max_grad_norm
+ * (g <- g min(1, max_grad_norm / (||g||_2 + 1e-6)), the norm taken over all
+ * groups of the call; max_grad_norm <= 0 disables clipping), with the
+ * learning rate of step t (1-based) lr_max * (t-1)/W during the first W =
+ * warmup_steps steps and lr_max * (N - (t-1)) / (N - W) after them, never
+ * below zero (N = total_steps).  The paper's setting: betas (0.9, 0.95),
+ * weight decay 0, clipping at 1.0, W = N / 10, separate maximum learning
+ * rates for A, B and for s.
+ * Each group is a contiguous float32 range of n elements (param, grad and
+ * the two moment buffers, all device pointers; moments start at zero) with
+ * its own lr_max and weight_decay; at most 32 groups per call (keep a
+ * model's adapters in one buffer).  grad_norm_out (device float, nullable)
+ * receives the norm before clipping.  Deterministic.  ws: at least
+ * lrqat_adamw_workspace_size() bytes.
+ */
+typedef struct {
+  float* param;
+  const float* grad;
+  float* exp_avg;
+  float* exp_avg_sq;
+  int64_t n;
+  float lr_max;
+  float weight_decay;
+} lrqat_param_group;
+
+typedef struct {
+  float beta1, beta2, eps;
+  float max_grad_norm;
+  int64_t total_steps, warmup_steps;
+} lrqat_adamw_config;
+
+size_t lrqat_adamw_workspace_size(int n_groups, const lrqat_param_group* groups);
+lrqat_status lrqat_adamw_step(const lrqat_adamw_config* cfg, int64_t step, int n_groups,
+                              const lrqat_param_group* groups, float* grad_norm_out, void* ws,
+                              size_t ws_bytes, void* stream);
+
 /* Human-readable name of a status code (static string). */
 const char* lrqat_status_string(lrqat_status status);
 

@@ -536,6 +536,66 @@ lrqat_status lrqat_infer_forward(const lrqat_layer* layer, int64_t tokens, const
   return weight_gemm_forward(di, tokens, X, q, ldq, s, z, Y, base, w, st);
 }
 
+static lrqat_status adamw_args(const lrqat_adamw_config* cfg, int n_groups, const lrqat_param_group* groups,
+                               OptimArgs& a) {
+  if (!cfg) return fail(LRQAT_EINVAL, "config is NULL");
+  if (n_groups < 0 || n_groups > kMaxOptimGroups)
+    return fail(LRQAT_EINVAL, "n_groups must be in [0, %d] (got %d)", kMaxOptimGroups, n_groups);
+  if (n_groups && !groups) return fail(LRQAT_EINVAL, "groups is NULL");
+  if (!(cfg->beta1 >= 0.f && cfg->beta1 < 1.f && cfg->beta2 >= 0.f && cfg->beta2 < 1.f))
+    return fail(LRQAT_EINVAL, "betas must be in [0, 1)");
+  if (!(cfg->eps >= 0.f) || !std::isfinite(cfg->eps) || !std::isfinite(cfg->max_grad_norm))
+    return fail(LRQAT_EINVAL, "eps and max_grad_norm must be finite, eps >= 0");
+  if (cfg->total_steps < 1 || cfg->warmup_steps < 0 || cfg->warmup_steps > cfg->total_steps)
+    return fail(LRQAT_EINVAL, "need 0 <= warmup_steps <= total_steps and total_steps >= 1");
+  a = OptimArgs{};
+  a.ngroups = n_groups;
+  a.total = cfg->total_steps;
+  a.warmup = cfg->warmup_steps;
+  a.beta1 = cfg->beta1;
+  a.beta2 = cfg->beta2;
+  a.eps = cfg->eps;
+  a.max_norm = cfg->max_grad_norm;
+  for (int i = 0; i < n_groups; ++i) {
+    const lrqat_param_group& g = groups[i];
+    if (g.n < 0) return fail(LRQAT_EINVAL, "group %d: n < 0", i);
+    if (g.n > 0 && (!g.param || !g.grad || !g.exp_avg || !g.exp_avg_sq))
+      return fail(LRQAT_EINVAL, "group %d: a NULL tensor", i);
+    if (!aligned(g.param, 4) || !aligned(g.grad, 4) || !aligned(g.exp_avg, 4) || !aligned(g.exp_avg_sq, 4))
+      return fail(LRQAT_EINVAL, "group %d: tensors must be 4-byte aligned", i);
+    if (!std::isfinite(g.lr_max) || !std::isfinite(g.weight_decay))
+      return fail(LRQAT_EINVAL, "group %d: lr_max and weight_decay must be finite", i);
+    a.g[i] = OptimGroup{g.param, g.grad, g.exp_avg, g.exp_avg_sq, g.n, g.lr_max, g.weight_decay};
+  }
+  optim_prepare(a);
+  return LRQAT_OK;
+}
+
+size_t lrqat_adamw_workspace_size(int n_groups, const lrqat_param_group* groups) {
+  lrqat_adamw_config cfg{0.9f, 0.95f, 1e-8f, 1.f, 1, 0};
+  OptimArgs a;
+  if (adamw_args(&cfg, n_groups, groups, a) != LRQAT_OK) return 0;
+  return size_t(round_up(int64_t(optim_chunks(a) * 8 + 16), 256));
+}
+
+lrqat_status lrqat_adamw_step(const lrqat_adamw_config* cfg, int64_t step, int n_groups,
+                              const lrqat_param_group* groups, float* grad_norm_out, void* ws, size_t ws_bytes,
+                              void* stream) {
+  OptimArgs a;
+  LRQAT_TRY(adamw_args(cfg, n_groups, groups, a));
+  if (step < 1) return fail(LRQAT_EINVAL, "step is 1-based (got %lld)", (long long)step);
+  a.step = step;
+  if (grad_norm_out && !aligned(grad_norm_out, 4)) return fail(LRQAT_EINVAL, "grad_norm_out is not 4-byte aligned");
+  NEED(ws, 256);
+  const size_t need = size_t(round_up(int64_t(optim_chunks(a) * 8 + 16), 256));
+  if (ws_bytes < need) return fail(LRQAT_EWORKSPACE, "workspace of %zu bytes is smaller than the %zu bytes needed",
+                                   ws_bytes, need);
+  double* part = reinterpret_cast<double*>(static_cast<uint8_t*>(ws) + 16);
+  float* norm_coef = static_cast<float*>(ws);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  return hip_status(timed("adamw", st, [&] { return launch_adamw(a, part, norm_coef, grad_norm_out, st); }), "adamw");
+}
+
 const char* lrqat_status_string(lrqat_status status) {
   switch (status) {
     case LRQAT_OK: return "LRQAT_OK";

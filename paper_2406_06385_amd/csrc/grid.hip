@@ -116,10 +116,13 @@ __global__ __launch_bounds__(256) void k_encode(const float* __restrict__ W0, co
 //
 // Error bound of the float32 delta: the split drops terms below
 // 3.0001 * 2^-16 |a||b| per product; float32 accumulation of the 3r products
-// and the scaling by c add at most (3r + 2) 2^-24 sum |products|.  With
-// Cauchy-Schwarz, sum_rho |A_i,rho||B_rho,j| <= ||A_i:|| ||B_:j||, so
-// |delta32 - delta| <= tau_coef * ||A_i:|| * max_j ||B_:j||, where tau_coef =
-// 1.02 (3 * 2^-16 + (3r + 2) 2^-24) |c| (the 1.02 covers the float32 norms).
+// and the scaling by c add at most (3r + 2) 2^-23 sum |products| -- one unit
+// in the last place per addition, which also covers an accumulator that
+// truncates instead of rounding to nearest (the MFMA's internal rounding is
+// not specified).  With Cauchy-Schwarz, sum_rho |A_i,rho||B_rho,j| <=
+// ||A_i:|| ||B_:j||, so |delta32 - delta| <= tau_coef * ||A_i:|| *
+// max_j ||B_:j||, where tau_coef = 1.02 (3 * 2^-16 + (3r + 2) 2^-23) |c|
+// (the 1.02 covers the float32 norms).
 // Near a decision point n != 0 the float32 sum u - n adds at most 2^-23 |n|;
 // near n = 0 it is exact.  Elements inside that bound are decided again from
 // a float64 delta, so the grid equals the exact one except within float64
@@ -757,7 +760,7 @@ hipError_t launch_grid(const GridArgs& a0, hipStream_t st) {
   a.nit = 8;
   while (a.nit > 1 && nstrips * ((nrb + a.nit - 1) / a.nit) < GR_MIN_BLOCKS) a.nit /= 2;
   const int64_t nblocks = nstrips * ((nrb + a.nit - 1) / a.nit);
-  a.tau_coef = float(1.02 * (3.0 * 0x1p-16 + (3.0 * a.r + 2.0) * 0x1p-24) * (a.c < 0 ? -a.c : a.c));
+  a.tau_coef = float(1.02 * (3.0 * 0x1p-16 + (3.0 * a.r + 2.0) * 0x1p-23) * (a.c < 0 ? -a.c : a.c));
   const unsigned nb = unsigned(nblocks);
   const bool coal = a.r == 32 && a.k % 4 == 0 && (reinterpret_cast<uintptr_t>(a.A) & 15) == 0 &&
                     (reinterpret_cast<uintptr_t>(a.B) & 15) == 0;

@@ -124,4 +124,25 @@ hipError_t launch_f32_forward(const F32Args& a, float* Y, hipStream_t st);
 hipError_t launch_f32_dx(const F32Args& a, float* dX, hipStream_t st);
 hipError_t launch_f32_dw(const F32Args& a, float* dA, float* dB, float* ds, int accumulate, hipStream_t st);
 
+// AdamW step with global L2 clipping (optim.hip).
+struct OptimGroup {
+  float* param;
+  const float* grad;
+  float* exp_avg;
+  float* exp_avg_sq;
+  int64_t n;
+  float lr_max, weight_decay;
+};
+constexpr int kMaxOptimGroups = 32;
+struct OptimArgs {
+  OptimGroup g[kMaxOptimGroups];
+  int64_t first[kMaxOptimGroups + 1];  // first chunk of each group (set by optim_prepare)
+  int ngroups;
+  int64_t step, total, warmup;
+  float beta1, beta2, eps, max_norm;
+};
+void optim_prepare(OptimArgs& a);
+int64_t optim_chunks(const OptimArgs& a);
+hipError_t launch_adamw(const OptimArgs& a, double* part, float* norm_coef, float* norm_out, hipStream_t st);
+
 }  // namespace lrqat

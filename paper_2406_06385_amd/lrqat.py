@@ -29,6 +29,17 @@ class _Layer(ctypes.Structure):
                 ("act_bits", ctypes.c_int32), ("act_dtype", ctypes.c_int32)]
 
 
+class _ParamGroup(ctypes.Structure):
+    _fields_ = [("param", ctypes.c_void_p), ("grad", ctypes.c_void_p), ("exp_avg", ctypes.c_void_p),
+                ("exp_avg_sq", ctypes.c_void_p), ("n", ctypes.c_int64), ("lr_max", ctypes.c_float),
+                ("weight_decay", ctypes.c_float)]
+
+
+class _AdamWConfig(ctypes.Structure):
+    _fields_ = [("beta1", ctypes.c_float), ("beta2", ctypes.c_float), ("eps", ctypes.c_float),
+                ("max_grad_norm", ctypes.c_float), ("total_steps", ctypes.c_int64), ("warmup_steps", ctypes.c_int64)]
+
+
 @dataclass(frozen=True)
 class LayerSpec:
     """Hyper-parameters of one LR-QAT linear (mirrors the C struct lrqat_layer)."""
@@ -96,6 +107,11 @@ def _lib():
         for fn in ("lrqat_init_from_weights", "lrqat_forward", "lrqat_backward", "lrqat_backward_static",
                    "lrqat_merge_to_int4", "lrqat_infer_forward"):
             getattr(lib, fn).restype = ctypes.c_int
+        PG = ctypes.POINTER(_ParamGroup)
+        lib.lrqat_adamw_workspace_size.argtypes = [ctypes.c_int, PG]
+        lib.lrqat_adamw_workspace_size.restype = SZ
+        lib.lrqat_adamw_step.argtypes = [ctypes.POINTER(_AdamWConfig), I64, ctypes.c_int, PG, P, P, SZ, P]
+        lib.lrqat_adamw_step.restype = ctypes.c_int
         lib.lrqat_status_string.argtypes = [ctypes.c_int]
         lib.lrqat_status_string.restype = ctypes.c_char_p
         lib.lrqat_last_error.restype = ctypes.c_char_p
@@ -322,6 +338,41 @@ def lrqat_infer_forward(spec: LayerSpec, X, W_int4, s, z=None, Y=None, ws=None, 
     _check(_lib().lrqat_infer_forward(ctypes.byref(L), T, _ptr(X), _ptr(W_int4), _ptr(s), _ptr(z), _ptr(Y),
                                       _ptr(ws), ws.numel(), _stream(st)))
     return Y
+
+
+def _groups(groups):
+    arr = (_ParamGroup * max(1, len(groups)))()
+    dev = None
+    for i, g in enumerate(groups):
+        p = g["param"]
+        dev = dev or p.device
+        n = p.numel()
+        for key in ("param", "grad", "exp_avg", "exp_avg_sq"):
+            _expect(g[key], tuple(p.shape), torch.float32, key, dev)
+        arr[i] = _ParamGroup(g["param"].data_ptr(), g["grad"].data_ptr(), g["exp_avg"].data_ptr(),
+                             g["exp_avg_sq"].data_ptr(), n, float(g["lr_max"]), float(g.get("weight_decay", 0.0)))
+    return arr, dev
+
+
+def lrqat_adamw_step(groups, step, total_steps, warmup_steps, beta1=0.9, beta2=0.95, eps=1e-8, max_grad_norm=1.0,
+                     grad_norm=None, ws=None, stream=None):
+    """AdamW with global L2 clipping and the linear warm-up/decay schedule, in place.
+    groups: list of dicts with float32 tensors param, grad, exp_avg, exp_avg_sq (same
+    shape) and floats lr_max, weight_decay.  grad_norm: optional float32 [1] tensor
+    receiving the norm before clipping."""
+    arr, dev = _groups(groups)
+    cfg = _AdamWConfig(beta1, beta2, eps, max_grad_norm, int(total_steps), int(warmup_steps))
+    st = _torch_stream(stream)
+    if ws is None:
+        n = _lib().lrqat_adamw_workspace_size(len(groups), arr)
+        if n == 0:
+            raise LRQATError(LRQAT_EINVAL, _lib().lrqat_last_error().decode())
+        with torch.cuda.stream(st):
+            ws = workspace(n, dev or "cuda")
+    if grad_norm is not None:
+        _expect(grad_norm, (1,), torch.float32, "grad_norm", dev)
+    _check(_lib().lrqat_adamw_step(ctypes.byref(cfg), int(step), len(groups), arr, _ptr(grad_norm), _ptr(ws),
+                                   ws.numel(), _stream(st)))
 
 
 def lrqat_timing_enable(on: bool = True):

@@ -233,3 +233,54 @@ def test_inference_on_merged_weights(lr, case):
     assert_close(errs, tol)
     # the training-time forward of the same layer gives the same bits (same GEMM, same grid)
     assert torch.equal(Y.view(torch.int16), Yt.view(torch.int16))
+
+
+# ----------------------------------------------------------------------------- optimizer step
+
+def test_adamw_with_clipping_and_schedule(lr):
+    """Several AdamW steps on three groups (A, B and s of a 4096 x 4096 layer,
+    separate maximum learning rates, weight decay on one, a misaligned group for
+    the scalar path) against the oracle from the same float32 start: parameters,
+    both moments and the pre-clip norm."""
+    m, k, r = 4096, 4096, 32
+    rng = np.random.default_rng(7)
+    shapes = [(m, r), (r, k), (m - 1,)]
+    lr_max = [1e-3, 1e-3, 1e-5]
+    wd = [0.0, 0.1, 0.0]
+    total, warm = 100, 10
+    host = [dict(p=rng.normal(0, 0.05, size=sh).astype(np.float32), m=np.zeros(sh), v=np.zeros(sh)) for sh in shapes]
+    dev = []
+    for i, (h, sh) in enumerate(zip(host, shapes)):
+        if i == 2:  # a float32 view one element into its buffer: 4-byte but not 16-byte aligned
+            buf = torch.zeros(int(np.prod(sh)) + 1, dtype=torch.float32, device="cuda")
+            P = buf[1:]
+            P.copy_(torch.from_numpy(h["p"]))
+        else:
+            P = torch.from_numpy(h["p"].copy()).cuda()
+        dev.append(dict(param=P, grad=torch.empty_like(P), exp_avg=torch.zeros_like(P),
+                        exp_avg_sq=torch.zeros_like(P), lr_max=lr_max[i], weight_decay=wd[i]))
+    host_p = [h["p"].astype(np.float64) for h in host]
+    norm = torch.zeros(1, dtype=torch.float32, device="cuda")
+    for step, gscale in ((1, 1.0), (2, 3e-3), (3, 1.0), (4, 0.5), (57, 2.0), (58, 1e-3)):
+        grads = [rng.normal(0, 1.0, size=sh).astype(np.float32) * np.float32(gscale / np.sqrt(np.prod(sh)))
+                 for sh in shapes]
+        for d, g in zip(dev, grads):
+            d["grad"].copy_(torch.from_numpy(g))
+        lr.lrqat_adamw_step(dev, step, total, warm, grad_norm=norm)
+        coef, gn = O.clip_coefficient(grads, 1.0)
+        for i in range(3):
+            lr_t = O.lr_at(step, lr_max[i], total, warm)
+            host_p[i], host[i]["m"], host[i]["v"] = O.adamw_step(host_p[i], grads[i], host[i]["m"], host[i]["v"], step,
+                                                                 lr_t, 0.9, 0.95, 1e-8, wd[i], clip=coef)
+        torch.cuda.synchronize()
+        assert abs(float(norm[0]) - gn) <= 1e-6 * gn, (step, float(norm[0]), gn)
+        _log(f"[adamw step {step}] norm {gn:.4g} clip {coef:.4g}")
+        for i in range(3):
+            p_dev = dev[i]["param"].cpu().numpy().astype(np.float64)
+            m_dev = dev[i]["exp_avg"].cpu().numpy().astype(np.float64)
+            v_dev = dev[i]["exp_avg_sq"].cpu().numpy().astype(np.float64)
+            ep = np.abs(p_dev - host_p[i]).max()
+            bound = 8 * 2.0 ** -24 * np.abs(host_p[i]).max() + 1e-5 * lr_max[i]
+            assert ep <= bound, (step, i, ep, bound)
+            for name, a, b in (("m", m_dev, host[i]["m"]), ("v", v_dev, host[i]["v"])):
+                assert np.abs(a - b).max() <= 1e-5 * np.abs(b).max() + 1e-30, (step, i, name)
