@@ -115,6 +115,40 @@ lrqat_status lrqat_init_from_weights(const lrqat_layer* layer, const float* W0,
                                      float* s0_out, int32_t* z0_out, void* phi0_out, void* stream);
 
 /*
+ * Setup with L^p-norm range estimation (Section 4 'Baselines', Appendix B
+ * 'PTQ initialization': the range minimising the L^p norm between quantized
+ * and unquantized weights, p in {2, 2.4, 3, 3.5, 4, 5} in the paper).  For
+ * each row (or row-group) the candidates are the clipping ratios j / n_grid,
+ * j = 1..n_grid, of the min-max range, s_j = (j / n_grid) max|W0| /
+ * (2^(b-1)-1) in float32, with error E_j = sum |W0 - s_j clip(round(W0 /
+ * s_j))|^p (float32 terms, float64 sums); the smallest j of the minimal E_j
+ * gives s0.  Then Phi0 = phi(W0 / s0) as in lrqat_init_from_weights.
+ * 1 <= p <= 16, 1 <= n_grid <= 10000; a row or group holds at most 16384
+ * weights.
+ */
+lrqat_status lrqat_init_lp(const lrqat_layer* layer, const float* W0, float p, int n_grid,
+                           float* s0_out, void* phi0_out, void* stream);
+
+/*
+ * LoftQ initialisation with one alternating step (Section 3 'Downcasting
+ * operator', Section 4.2 ablation): for INT-b Phi0 (phi_format
+ * LRQAT_PHI_INT_PACKED2) from W0 and a given scale s0 (min-max or L^p), with
+ * x = W0 / s0: Phi0 = clip(round(x)), and A [m][r], B [r][k] whose product
+ * (alpha/r) A B approximates the dropped fractional part R = x - Phi0 by
+ * its best rank-r approximation, split evenly (A^T A = B B^T).  The
+ * approximation comes from randomized subspace iteration (r + 16 columns,
+ * n_iter iterations, CholeskyQR2 orthonormalisation, Jacobi on the small
+ * Gram matrix; 32 iterations capture over 99.9% of the optimal rank-r energy
+ * of a noise-like R).  sigma_out (nullable): the r singular values found.
+ * rank <= 48, alpha / r > 0.  ws: lrqat_init_loftq_workspace_size() bytes
+ * (R in float32 plus the subspace blocks).
+ */
+size_t lrqat_init_loftq_workspace_size(const lrqat_layer* layer);
+lrqat_status lrqat_init_loftq(const lrqat_layer* layer, const float* W0, const float* s0, int n_iter,
+                              void* phi0_out, float* A_out, float* B_out, float* sigma_out, void* ws,
+                              size_t ws_bytes, void* stream);
+
+/*
  * Forward pass (Section 3, Eq. lr_qat): Y = X_hat * W_hat^T.
  *   X     [T][k] act_dtype     layer input (X_hat = X, or its int8 fake
  *                               quantisation when act_bits = 8)

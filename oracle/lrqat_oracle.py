@@ -428,21 +428,34 @@ def lp_scale_search(W0: np.ndarray, bits: int, group_size: int, p: float, n_grid
     m, k = W.shape
     lo, hi = grid_limits(bits)
     Wg = W.reshape(m, 1, k) if group_size == 0 else W.reshape(m, k // group_size, group_size)
-    amax = np.abs(Wg).max(axis=2)
-    E = np.empty(amax.shape + (n_grid,), np.float64)
-    S = np.empty(amax.shape + (n_grid,), np.float32)
+    S = lp_candidate_scales(W0, bits, group_size, n_grid).reshape(Wg.shape[:2] + (n_grid,))
+    E = np.empty(S.shape, np.float64)
     for j in range(1, n_grid + 1):
-        sj = ((np.float32(j) / np.float32(n_grid)) * amax / np.float32(hi)).astype(np.float32)
-        sj = np.where(amax > 0, sj, np.float32(1.0)).astype(np.float32)
+        sj = S[..., j - 1]
         qv = np.clip(np.rint((Wg / sj[..., None]).astype(np.float32)), lo, hi)
         err = np.abs(Wg.astype(np.float64) - sj[..., None].astype(np.float64) * qv)
         E[..., j - 1] = np.sum(err ** p, axis=2)
-        S[..., j - 1] = sj
     jbest = np.argmin(E, axis=-1)
     s0 = np.take_along_axis(S, jbest[..., None], axis=-1)[..., 0]
     if group_size == 0:
         return s0.reshape(m), (jbest + 1).reshape(m).astype(np.int32), E.reshape(m, n_grid)
     return s0, (jbest + 1).astype(np.int32), E
+
+
+def lp_candidate_scales(W0: np.ndarray, bits: int, group_size: int, n_grid: int = 100) -> np.ndarray:
+    """The candidate scales s_j = fl32(fl32(j / n_grid) max|W| / (2^(b-1) - 1)),
+    j = 1..n_grid, of every row (or row-group): float32 [m][n_grid] or
+    [m][k/g][n_grid] (an all-zero row or group gets 1)."""
+    W = np.asarray(W0, dtype=np.float32)
+    m, k = W.shape
+    _, hi = grid_limits(bits)
+    Wg = W.reshape(m, 1, k) if group_size == 0 else W.reshape(m, k // group_size, group_size)
+    amax = np.abs(Wg).max(axis=2)
+    S = np.empty(amax.shape + (n_grid,), np.float32)
+    for j in range(1, n_grid + 1):
+        sj = ((np.float32(j) / np.float32(n_grid)) * amax / np.float32(hi)).astype(np.float32)
+        S[..., j - 1] = np.where(amax > 0, sj, np.float32(1.0)).astype(np.float32)
+    return S.reshape(m, n_grid) if group_size == 0 else S
 
 
 def loftq_init(W0: np.ndarray, s0: np.ndarray, bits: int, group_size: int, rank: int, alpha: float):

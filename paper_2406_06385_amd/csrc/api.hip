@@ -10,6 +10,7 @@
 #include <string>
 #include <vector>
 
+#include "init.h"
 #include "kernels.h"
 #include "lrqat.h"
 
@@ -78,6 +79,7 @@ struct Dims {
   int q8w;  // the integer grid is kept as int8 (fixed-point Phi0 with b = 5..7)
   float c;
   double c64;
+  bool alpha_nonpos() const { return !(c64 > 0.0); }
 };
 
 struct Workspace {
@@ -489,6 +491,72 @@ lrqat_status lrqat_merge_to_int4(const lrqat_layer* layer, const void* phi0, con
   ga.kq = d.k;
   LRQAT_TRY(hip_status(timed("merge", st, [&] { return launch_grid(ga, st); }), "merge"));
   return LRQAT_OK;
+}
+
+lrqat_status lrqat_init_lp(const lrqat_layer* layer, const float* W0, float p, int n_grid, float* s0_out,
+                           void* phi0_out, void* stream) {
+  Dims d;
+  LRQAT_TRY(check_layer(layer, d));
+  NEED(W0, 4);
+  NEED(s0_out, 4);
+  NEED(phi0_out, 16);
+  if (!(p >= 1.f && p <= 16.f)) return fail(LRQAT_EINVAL, "p must be in [1, 16] (got %g)", double(p));
+  if (n_grid < 1 || n_grid > 10000) return fail(LRQAT_EINVAL, "n_grid must be in [1, 10000] (got %d)", n_grid);
+  const int64_t gsize = d.g ? d.g : d.k;
+  if (gsize > kLpMaxGroup)
+    return fail(LRQAT_EUNSUPPORTED, "the L^p search holds a row or group of at most %lld weights (got %lld)",
+                (long long)kLpMaxGroup, (long long)gsize);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  LRQAT_TRY(hip_status(timed("init_lp", st, [&] {
+                         return launch_lp_search(W0, d.m, d.k, gsize, d.bits, p, n_grid, s0_out, nullptr, st);
+                       }), "init_lp"));
+  LRQAT_TRY(hip_status(timed("init_encode", st, [&] {
+                         return launch_encode(W0, s0_out, nullptr, d.m, d.k, gsize, d.bits, d.packed, phi0_out, st);
+                       }), "init_encode"));
+  return LRQAT_OK;
+}
+
+static lrqat_status loftq_dims(const lrqat_layer* layer, Dims& d, int& l) {
+  LRQAT_TRY(check_layer(layer, d));
+  if (!d.packed) return fail(LRQAT_EINVAL, "LoftQ initialisation writes INT-b Phi0: phi_format must be INT_PACKED2");
+  if (d.r > kLoftqMaxRank)
+    return fail(LRQAT_EUNSUPPORTED, "LoftQ initialisation runs ranks up to %d (got %lld)", kLoftqMaxRank,
+                (long long)d.r);
+  l = int(std::min<int64_t>(d.r + kLoftqOversample, std::min(d.m, d.k)));
+  if (l < d.r) return fail(LRQAT_EINVAL, "rank %lld exceeds min(m, k)", (long long)d.r);
+  if (d.alpha_nonpos()) return fail(LRQAT_EINVAL, "LoftQ initialisation needs alpha / r > 0");
+  return LRQAT_OK;
+}
+
+size_t lrqat_init_loftq_workspace_size(const lrqat_layer* layer) {
+  Dims d;
+  int l = 0;
+  if (loftq_dims(layer, d, l) != LRQAT_OK) return 0;
+  return loftq_workspace(d.m, d.k, l);
+}
+
+lrqat_status lrqat_init_loftq(const lrqat_layer* layer, const float* W0, const float* s0, int n_iter, void* phi0_out,
+                              float* A_out, float* B_out, float* sigma_out, void* ws, size_t ws_bytes, void* stream) {
+  Dims d;
+  int l = 0;
+  LRQAT_TRY(loftq_dims(layer, d, l));
+  NEED(W0, 4);
+  NEED(s0, 4);
+  NEED(phi0_out, 16);
+  NEED(A_out, 4);
+  NEED(B_out, 4);
+  if (sigma_out && !aligned(sigma_out, 4)) return fail(LRQAT_EINVAL, "sigma_out is not 4-byte aligned");
+  if (n_iter < 0 || n_iter > 1000) return fail(LRQAT_EINVAL, "n_iter must be in [0, 1000] (got %d)", n_iter);
+  NEED(ws, 256);
+  const size_t need = loftq_workspace(d.m, d.k, l);
+  if (ws_bytes < need)
+    return fail(LRQAT_EWORKSPACE, "workspace of %zu bytes is smaller than the %zu bytes needed", ws_bytes, need);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const int64_t gsize = d.g ? d.g : d.k;
+  return hip_status(timed("init_loftq", st, [&] {
+                      return launch_loftq(W0, s0, d.m, d.k, gsize, d.bits, int(d.r), l, d.c64, n_iter,
+                                          static_cast<uint8_t*>(phi0_out), A_out, B_out, sigma_out, ws, st);
+                    }), "init_loftq");
 }
 
 size_t lrqat_infer_workspace_size(const lrqat_layer* layer, int64_t tokens) {

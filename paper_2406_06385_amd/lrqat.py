@@ -107,6 +107,12 @@ def _lib():
         for fn in ("lrqat_init_from_weights", "lrqat_forward", "lrqat_backward", "lrqat_backward_static",
                    "lrqat_merge_to_int4", "lrqat_infer_forward"):
             getattr(lib, fn).restype = ctypes.c_int
+        lib.lrqat_init_lp.argtypes = [F, P, ctypes.c_float, ctypes.c_int, P, P, P]
+        lib.lrqat_init_lp.restype = ctypes.c_int
+        lib.lrqat_init_loftq_workspace_size.argtypes = [F]
+        lib.lrqat_init_loftq_workspace_size.restype = SZ
+        lib.lrqat_init_loftq.argtypes = [F, P, P, ctypes.c_int, P, P, P, P, P, SZ, P]
+        lib.lrqat_init_loftq.restype = ctypes.c_int
         PG = ctypes.POINTER(_ParamGroup)
         lib.lrqat_adamw_workspace_size.argtypes = [ctypes.c_int, PG]
         lib.lrqat_adamw_workspace_size.restype = SZ
@@ -208,6 +214,40 @@ def lrqat_init_from_weights(spec: LayerSpec, W0: torch.Tensor, stream=None, asym
     L = spec.c_struct()
     _check(_lib().lrqat_init_from_weights(ctypes.byref(L), _ptr(W0), _ptr(s0), _ptr(z0), _ptr(phi0), _stream(st)))
     return (s0, z0, phi0) if asymmetric else (s0, phi0)
+
+
+def lrqat_init_lp(spec: LayerSpec, W0: torch.Tensor, p: float, n_grid: int = 100, stream=None):
+    """-> (s0, Phi0) with s0 from the L^p-norm range search over n_grid clipping ratios."""
+    _expect(W0, (spec.out_features, spec.in_features), torch.float32, "W0")
+    st = _torch_stream(stream)
+    with torch.cuda.stream(st):
+        s0 = torch.empty(spec.scale_shape(), dtype=torch.float32, device=W0.device)
+        phi0 = torch.empty(spec.phi_shape(), dtype=spec.phi_dtype, device=W0.device)
+    L = spec.c_struct()
+    _check(_lib().lrqat_init_lp(ctypes.byref(L), _ptr(W0), float(p), int(n_grid), _ptr(s0), _ptr(phi0), _stream(st)))
+    return s0, phi0
+
+
+def lrqat_init_loftq(spec: LayerSpec, W0: torch.Tensor, s0: torch.Tensor, n_iter: int = 32, stream=None):
+    """-> (Phi0 packed INT-b, A, B, sigma) of the LoftQ (T = 1) initialisation for the given scale."""
+    m, k, r = spec.out_features, spec.in_features, spec.rank
+    _expect(W0, (m, k), torch.float32, "W0")
+    dev = W0.device
+    _expect(s0, spec.scale_shape(), torch.float32, "s0", dev)
+    L = spec.c_struct()
+    n = _lib().lrqat_init_loftq_workspace_size(ctypes.byref(L))
+    if n == 0:
+        raise LRQATError(LRQAT_EINVAL, _lib().lrqat_last_error().decode())
+    st = _torch_stream(stream)
+    with torch.cuda.stream(st):
+        phi0 = torch.empty(spec.phi_shape(), dtype=spec.phi_dtype, device=dev)
+        A = torch.empty((m, r), dtype=torch.float32, device=dev)
+        B = torch.empty((r, k), dtype=torch.float32, device=dev)
+        sigma = torch.empty(r, dtype=torch.float32, device=dev)
+        ws = workspace(n, dev)
+    _check(_lib().lrqat_init_loftq(ctypes.byref(L), _ptr(W0), _ptr(s0), int(n_iter), _ptr(phi0), _ptr(A), _ptr(B),
+                                   _ptr(sigma), _ptr(ws), ws.numel(), _stream(st)))
+    return phi0, A, B, sigma
 
 
 def lrqat_forward(spec: LayerSpec, X, phi0, s, A, B, Y=None, ws=None, stream=None, z=None):

@@ -284,3 +284,64 @@ def test_adamw_with_clipping_and_schedule(lr):
             assert ep <= bound, (step, i, ep, bound)
             for name, a, b in (("m", m_dev, host[i]["m"]), ("v", v_dev, host[i]["v"])):
                 assert np.abs(a - b).max() <= 1e-5 * np.abs(b).max() + 1e-30, (step, i, name)
+
+
+# ----------------------------------------------------------------------------- L^p range search and LoftQ
+
+@pytest.mark.parametrize("bits,g,p", [(4, 0, 2.0), (4, 0, 2.4), (3, 128, 4.0), (2, 64, 3.5)])
+def test_lp_range_search(lr, bits, g, p):
+    """The device's scale is one of the oracle's candidates s_j and a minimiser of
+    the oracle's error table (to 1e-6 relative: the kernel sums float32 terms);
+    Phi0 is the downcast with that scale, bit for bit."""
+    m, k, n_grid = 520, 768, 100
+    spec = lr.LayerSpec(m, k, 8, 8.0, bits, "q8", g, 0, "bf16")
+    W0 = I.gen_w0(m, k, 150 + bits, 151, 0.02, 0.01)
+    s_dev, phi_dev = lr.lrqat_init_lp(spec, torch.from_numpy(W0).cuda(), p, n_grid)
+    torch.cuda.synchronize()
+    s_dev = s_dev.cpu().numpy()
+    S = O.lp_candidate_scales(W0, bits, g, n_grid).reshape(-1, n_grid)
+    _, j_ref, E = O.lp_scale_search(W0, bits, g, p, n_grid)
+    E = E.reshape(-1, n_grid)
+    hit = S == s_dev.reshape(-1, 1)
+    assert hit.any(axis=1).all(), "the device's scale is not a candidate"
+    j_dev = hit.argmax(axis=1)
+    e_dev, e_min = E[np.arange(len(E)), j_dev], E.min(axis=1)
+    assert np.all(e_dev <= e_min * (1 + 1e-6)), float((e_dev / e_min).max())
+    same = float((j_dev + 1 == j_ref.reshape(-1)).mean())
+    _log(f"  same pick as the oracle for {100 * same:.2f}% of {len(E)} rows/groups")
+    assert np.array_equal(phi_dev.cpu().numpy(), O.encode_phi0(W0, s_dev.reshape(O.minmax_scale(W0, bits, g).shape),
+                                                               bits, "q8", g))
+
+
+@pytest.mark.parametrize("bits,r,alpha,structured", [(3, 32, 32.0, False), (4, 8, 1.0, False), (3, 4, 4.0, True)])
+def test_loftq_initialisation(lr, bits, r, alpha, structured):
+    m, k = 512, 768
+    W0 = I.gen_w0(m, k, 170 + r, 171, 0.02, 0.0)
+    s0 = O.minmax_scale(W0, bits, 0)
+    if structured:
+        # W0 / s0 = integers + a rank-4 fractional part, so the residual has a clear rank-4 component
+        rng = np.random.default_rng(3)
+        u, v = rng.normal(size=(m, 4)), rng.normal(size=(4, k))
+        frac = np.clip(0.12 * (u @ v) / 2.0, -0.45, 0.45)
+        ints = np.clip(np.rint(W0 / s0[:, None]), -3, 2)
+        W0 = ((ints + frac) * s0[:, None]).astype(np.float32)
+        s0 = O.minmax_scale(W0, bits, 0)
+    spec = lr.LayerSpec(m, k, r, alpha, bits, "int_packed2", 0, 0, "bf16")
+    phi, A, B, sig = lr.lrqat_init_loftq(spec, torch.from_numpy(W0).cuda(), torch.from_numpy(s0).cuda(), 32)
+    torch.cuda.synchronize()
+    phi_ref, A_ref, B_ref, R, S = O.loftq_init(W0, s0, bits, 0, r, alpha)
+    assert np.array_equal(phi.cpu().numpy(), phi_ref)
+    A, B = A.cpu().numpy().astype(np.float64), B.cpu().numpy().astype(np.float64)
+    c = alpha / r
+    P = c * (A @ B)
+    opt = float((S[:r] ** 2).sum())
+    captured = float(np.sum(P * R))  # <R, P>: the energy the rank-r term explains (= ||P||^2 at the optimum)
+    resid = float(np.linalg.norm(R - P) ** 2)
+    _log(f"  captured {captured / opt:.6f} of the optimal energy; residual {resid / (S[r:] ** 2).sum():.6f} of the optimum")
+    assert captured >= 0.995 * opt
+    assert resid <= (1 + 2e-3) * float((S[r:] ** 2).sum())
+    assert np.allclose(A.T @ A, B @ B.T, rtol=1e-3, atol=1e-3 * np.abs(A.T @ A).max())
+    assert np.allclose(sig.cpu().numpy(), S[:r], rtol=2e-2)
+    if structured:
+        P_ref = c * (A_ref @ B_ref)
+        assert np.linalg.norm(P - P_ref) <= 1e-2 * np.linalg.norm(P_ref)
