@@ -93,15 +93,15 @@ __device__ __forceinline__ void load_kc_bf16(RegsKc& R, const uint16_t* __restri
   for (int i = 0; i < 8; ++i) R.v[i] = VEC ? ld128(r, base + i * step) : ld8_bf16_scalar(r, base + i * step);
 }
 
+// Each operand tile is written to LDS as 8 16-byte stores per thread; the
+// *_one functions do store number w (0..7), so the main loop can spread them
+// between MFMA groups.
 template <bool VEC>
-__device__ __forceinline__ void store_kc(uint16_t* tile, const RegsKc& R, int64_t K) {
+__device__ __forceinline__ void store_kc_one(uint16_t* tile, const RegsKc& R, int64_t K, int i) {
   const int t = threadIdx.x;
-#pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    u32x4 v = R.v[i];
-    if (!VEC) v = mask_tail(v, R.kk, int(K));
-    *reinterpret_cast<u32x4*>(tile + tile_off((t >> 3) + 32 * i, t & 7)) = v;
-  }
+  u32x4 v = R.v[i];
+  if (!VEC) v = mask_tail(v, R.kk, int(K));
+  *reinterpret_cast<u32x4*>(tile + tile_off((t >> 3) + 32 * i, t & 7)) = v;
 }
 
 // ------------------------------------------------------------------ K-contiguous int8 source (W4A8 codes)
@@ -119,18 +119,15 @@ __device__ __forceinline__ void load_kc_i8(RegsKc8& R, const int8_t* __restrict_
   for (int i = 0; i < 8; ++i) R.v[i] = ld64(r, base + i * step);
 }
 
-__device__ __forceinline__ void store_kc_i8(uint16_t* tile, const RegsKc8& R) {
+__device__ __forceinline__ void store_kc_i8_one(uint16_t* tile, const RegsKc8& R, int i) {
   const int t = threadIdx.x;
+  u32x4 o;
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    u32x4 o;
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const uint32_t w = R.v[i][q >> 1];
-      o[q] = pack_bf16x2(float(sbyte(w, 2 * (q & 1))), float(sbyte(w, 2 * (q & 1) + 1)));
-    }
-    *reinterpret_cast<u32x4*>(tile + tile_off((t >> 3) + 32 * i, t & 7)) = o;
+  for (int q = 0; q < 4; ++q) {
+    const uint32_t w = R.v[i][q >> 1];
+    o[q] = pack_bf16x2(float(sbyte(w, 2 * (q & 1))), float(sbyte(w, 2 * (q & 1) + 1)));
   }
+  *reinterpret_cast<u32x4*>(tile + tile_off((t >> 3) + 32 * i, t & 7)) = o;
 }
 
 // ------------------------------------------------------------------ zero offsets
@@ -170,32 +167,27 @@ __device__ __forceinline__ void load_q_kc(RegsQKc& R, const GemmArgs& p, int64_t
 }
 
 template <bool GRP, bool ZP>
-__device__ __forceinline__ void store_q_kc(uint16_t* tile, const RegsQKc& R) {
+__device__ __forceinline__ void store_q_kc_one(uint16_t* tile, const RegsQKc& R, int w8) {
   const int t = threadIdx.x;
+  const int i = w8 >> 2, c = w8 & 3;  // row half, 16-byte chunk
+  const int row = (t >> 1) + 128 * i;
+  const uint32_t w = R.v[i][c];
+  u32x4 o;
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int row = (t >> 1) + 128 * i;
-#pragma unroll
-    for (int c = 0; c < 4; ++c) {
-      const uint32_t w = R.v[i][c];
-      u32x4 o;
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        int na = nibble(w, 2 * q), nb = nibble(w, 2 * q + 1);
-        if (ZP) {
-          na -= R.zi[i];
-          nb -= R.zi[i];
-        }
-        float a = float(na), b = float(nb);
-        if (GRP) {
-          a *= R.sc[i];
-          b *= R.sc[i];
-        }
-        o[q] = pack_bf16x2(a, b);
-      }
-      *reinterpret_cast<u32x4*>(tile + tile_off(row, 4 * (t & 1) + c)) = o;
+  for (int q = 0; q < 4; ++q) {
+    int na = nibble(w, 2 * q), nb = nibble(w, 2 * q + 1);
+    if (ZP) {
+      na -= R.zi[i];
+      nb -= R.zi[i];
     }
+    float a = float(na), b = float(nb);
+    if (GRP) {
+      a *= R.sc[i];
+      b *= R.sc[i];
+    }
+    o[q] = pack_bf16x2(a, b);
   }
+  *reinterpret_cast<u32x4*>(tile + tile_off(row, 4 * (t & 1) + c)) = o;
 }
 
 // ------------------------------------------------------------------ int8 q, K-contiguous (forward B, 5..7-bit grids)
@@ -228,28 +220,25 @@ __device__ __forceinline__ void load_q_kc8(RegsQKc8& R, const GemmArgs& p, int64
 }
 
 template <bool GRP, bool ZP>
-__device__ __forceinline__ void store_q_kc8(uint16_t* tile, const RegsQKc8& R) {
+__device__ __forceinline__ void store_q_kc8_one(uint16_t* tile, const RegsQKc8& R, int i) {
   const int t = threadIdx.x;
+  u32x4 o;
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    u32x4 o;
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const uint32_t w = R.v[i][q >> 1];
-      int na = sbyte(w, 2 * (q & 1)), nb = sbyte(w, 2 * (q & 1) + 1);
-      if (ZP) {
-        na -= R.zi[i];
-        nb -= R.zi[i];
-      }
-      float a = float(na), b = float(nb);
-      if (GRP) {
-        a *= R.sc[i];
-        b *= R.sc[i];
-      }
-      o[q] = pack_bf16x2(a, b);
+  for (int q = 0; q < 4; ++q) {
+    const uint32_t w = R.v[i][q >> 1];
+    int na = sbyte(w, 2 * (q & 1)), nb = sbyte(w, 2 * (q & 1) + 1);
+    if (ZP) {
+      na -= R.zi[i];
+      nb -= R.zi[i];
     }
-    *reinterpret_cast<u32x4*>(tile + tile_off((t >> 3) + 32 * i, t & 7)) = o;
+    float a = float(na), b = float(nb);
+    if (GRP) {
+      a *= R.sc[i];
+      b *= R.sc[i];
+    }
+    o[q] = pack_bf16x2(a, b);
   }
+  *reinterpret_cast<u32x4*>(tile + tile_off((t >> 3) + 32 * i, t & 7)) = o;
 }
 
 // ------------------------------------------------------------------ K-strided sources
@@ -308,23 +297,20 @@ __device__ __forceinline__ void load_q_ks(RegsQKs& R, const GemmArgs& p, int64_t
 }
 
 template <bool ZP>
-__device__ __forceinline__ void store_q_ks(uint16_t* tile, const RegsQKs& R) {
+__device__ __forceinline__ void store_q_ks_one(uint16_t* tile, const RegsQKs& R, int c) {
   const int t = threadIdx.x;
   const int kg = t & 7, a = t >> 3;
+  u32x4 o;
 #pragma unroll
-  for (int c = 0; c < 8; ++c) {
-    u32x4 o;
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      int na = nibble(R.w[2 * q], c), nb = nibble(R.w[2 * q + 1], c);
-      if (ZP) {
-        na -= R.zi[2 * q];
-        nb -= R.zi[2 * q + 1];
-      }
-      o[q] = pack_bf16x2(float(na) * R.sc[2 * q], float(nb) * R.sc[2 * q + 1]);
+  for (int q = 0; q < 4; ++q) {
+    int na = nibble(R.w[2 * q], c), nb = nibble(R.w[2 * q + 1], c);
+    if (ZP) {
+      na -= R.zi[2 * q];
+      nb -= R.zi[2 * q + 1];
     }
-    *reinterpret_cast<u32x4*>(tile + tile_off(8 * a + c, kg)) = o;
+    o[q] = pack_bf16x2(float(na) * R.sc[2 * q], float(nb) * R.sc[2 * q + 1]);
   }
+  *reinterpret_cast<u32x4*>(tile + tile_off(8 * a + c, kg)) = o;
 }
 
 // int8 q (dX B, 5..7-bit grids): 8 bytes (columns 8a .. 8a + 7) of each K-line.
@@ -347,23 +333,20 @@ __device__ __forceinline__ void load_q_ks8(RegsQKs8& R, const GemmArgs& p, int64
 }
 
 template <bool ZP>
-__device__ __forceinline__ void store_q_ks8(uint16_t* tile, const RegsQKs8& R) {
+__device__ __forceinline__ void store_q_ks8_one(uint16_t* tile, const RegsQKs8& R, int c) {
   const int t = threadIdx.x;
   const int kg = t & 7, a = t >> 3;
+  u32x4 o;
 #pragma unroll
-  for (int c = 0; c < 8; ++c) {
-    u32x4 o;
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      int na = sbyte(R.v[2 * q][c >> 2], c & 3), nb = sbyte(R.v[2 * q + 1][c >> 2], c & 3);
-      if (ZP) {
-        na -= R.zi[2 * q];
-        nb -= R.zi[2 * q + 1];
-      }
-      o[q] = pack_bf16x2(float(na) * R.sc[2 * q], float(nb) * R.sc[2 * q + 1]);
+  for (int q = 0; q < 4; ++q) {
+    int na = sbyte(R.v[2 * q][c >> 2], c & 3), nb = sbyte(R.v[2 * q + 1][c >> 2], c & 3);
+    if (ZP) {
+      na -= R.zi[2 * q];
+      nb -= R.zi[2 * q + 1];
     }
-    *reinterpret_cast<u32x4*>(tile + tile_off(8 * a + c, kg)) = o;
+    o[q] = pack_bf16x2(float(na) * R.sc[2 * q], float(nb) * R.sc[2 * q + 1]);
   }
+  *reinterpret_cast<u32x4*>(tile + tile_off(8 * a + c, kg)) = o;
 }
 
 // bfloat16 (dW A = dY, dW B = X): 16-byte vector per K-line.
@@ -382,19 +365,16 @@ __device__ __forceinline__ void load_ks_bf16(RegsKs& R, const uint16_t* __restri
   for (int e = 0; e < 8; ++e) R.v[e] = VEC ? ld128(r, base + e * step) : ld8_bf16_scalar(r, base + e * step);
 }
 
-__device__ __forceinline__ void store_ks_bf16(uint16_t* tile, const RegsKs& R) {
+__device__ __forceinline__ void store_ks_bf16_one(uint16_t* tile, const RegsKs& R, int c) {
   const int t = threadIdx.x;
   const int kg = t & 7, a = t >> 3;
+  u32x4 o;
 #pragma unroll
-  for (int c = 0; c < 8; ++c) {
-    u32x4 o;
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const uint32_t x = R.v[2 * q][c >> 1], y = R.v[2 * q + 1][c >> 1];
-      o[q] = (c & 1) ? perm_hi16(x, y) : perm_lo16(x, y);
-    }
-    *reinterpret_cast<u32x4*>(tile + tile_off(8 * a + c, kg)) = o;
+  for (int q = 0; q < 4; ++q) {
+    const uint32_t x = R.v[2 * q][c >> 1], y = R.v[2 * q + 1][c >> 1];
+    o[q] = (c & 1) ? perm_hi16(x, y) : perm_lo16(x, y);
   }
+  *reinterpret_cast<u32x4*>(tile + tile_off(8 * a + c, kg)) = o;
 }
 
 // ------------------------------------------------------------------ the kernel
@@ -402,6 +382,8 @@ __device__ __forceinline__ void store_ks_bf16(uint16_t* tile, const RegsKs& R) {
 template <int V, bool ACT, bool GRP, bool VEC, int OPT>
 struct Loader;
 
+// store_one(w): LDS store w of the tile held in registers, w = 0..7 for the A
+// operand and 8..15 for the B operand.
 template <bool ACT, bool GRP, bool VEC, int OPT>
 struct Loader<kFwd, ACT, GRP, VEC, OPT> {
   static constexpr bool ZP = (OPT & kOptZ) != 0, Q8 = (OPT & kOptQ8) != 0;
@@ -413,11 +395,14 @@ struct Loader<kFwd, ACT, GRP, VEC, OPT> {
     if constexpr (Q8) load_q_kc8<GRP, ZP>(rb, p, n0, k0);
     else load_q_kc<GRP, ZP>(rb, p, n0, k0);
   }
-  __device__ __forceinline__ void store(const GemmArgs& p, uint16_t* As, uint16_t* Bs) {
-    if constexpr (ACT) store_kc_i8(As, ra);
-    else store_kc<VEC>(As, ra, p.K);
-    if constexpr (Q8) store_q_kc8<GRP, ZP>(Bs, rb);
-    else store_q_kc<GRP, ZP>(Bs, rb);
+  __device__ __forceinline__ void store_one(const GemmArgs& p, uint16_t* As, uint16_t* Bs, int w) {
+    if (w < 8) {
+      if constexpr (ACT) store_kc_i8_one(As, ra, w);
+      else store_kc_one<VEC>(As, ra, p.K, w);
+    } else {
+      if constexpr (Q8) store_q_kc8_one<GRP, ZP>(Bs, rb, w - 8);
+      else store_q_kc_one<GRP, ZP>(Bs, rb, w - 8);
+    }
   }
 };
 
@@ -431,10 +416,13 @@ struct Loader<kDx, ACT, GRP, VEC, OPT> {
     if constexpr (Q8) load_q_ks8<GRP, ZP>(rb, p, n0, k0);
     else load_q_ks<GRP, ZP>(rb, p, n0, k0);
   }
-  __device__ __forceinline__ void store(const GemmArgs& p, uint16_t* As, uint16_t* Bs) {
-    store_kc<VEC>(As, ra, p.K);
-    if constexpr (Q8) store_q_ks8<ZP>(Bs, rb);
-    else store_q_ks<ZP>(Bs, rb);
+  __device__ __forceinline__ void store_one(const GemmArgs& p, uint16_t* As, uint16_t* Bs, int w) {
+    if (w < 8) {
+      store_kc_one<VEC>(As, ra, p.K, w);
+    } else {
+      if constexpr (Q8) store_q_ks8_one<ZP>(Bs, rb, w - 8);
+      else store_q_ks_one<ZP>(Bs, rb, w - 8);
+    }
   }
 };
 
@@ -446,9 +434,9 @@ struct Loader<kDw, ACT, GRP, VEC, OPT> {
     load_ks_bf16<VEC>(ra, static_cast<const uint16_t*>(p.a), p.lda, m0, k0, p.K);
     load_ks_bf16<VEC>(rb, static_cast<const uint16_t*>(p.b), p.ldb, n0, k0, p.K);
   }
-  __device__ __forceinline__ void store(const GemmArgs&, uint16_t* As, uint16_t* Bs) {
-    store_ks_bf16(As, ra);
-    store_ks_bf16(Bs, rb);
+  __device__ __forceinline__ void store_one(const GemmArgs&, uint16_t* As, uint16_t* Bs, int w) {
+    if (w < 8) store_ks_bf16_one(As, ra, w);
+    else store_ks_bf16_one(Bs, rb, w - 8);
   }
 };
 
@@ -482,14 +470,46 @@ __device__ __forceinline__ u32x4 frag_tr_g(const uint16_t* tile, int c0, int k0,
   return u32x4{lo[0], lo[1], hi[0], hi[1]};
 }
 
-// Instruction interleave of one K-tile (one scheduling region): the first
-// k-step's fragment reads, then each MFMA followed by a few VALU ops of the
-// next tile's conversion; the fragment reads of the following k-step ride on
-// the first MFMAs of each k-step, the LDS writes of the next tile and the
-// global loads of the tile after it are spread over the whole sequence.
+// Instruction interleave of one k-step (16 MFMAs, one scheduling region
+// closed by a sched_barrier): each MFMA is followed by a few VALU ops of the
+// next tile's conversion; the 8 fragment reads of the following k-step ride on
+// the first MFMAs, the LDS stores of the next tile and the global loads of
+// the tile after it are spread over the sequence.
 enum : int { SG_VALU = 0x2, SG_MFMA = 0x8, SG_VMEM_READ = 0x20, SG_DS_READ = 0x100, SG_DS_WRITE = 0x200 };
 
-__device__ __forceinline__ void interleave() {
+// Schedules of the main loop, per GEMM, chosen by timing variants against
+// each other on the 4096 x 4096, T = 8192 layer (same process, interleaved
+// repeats): the pipeline, the k-step that issues the next tile's global loads,
+// and for one k-step the VALU ops after each MFMA, LDS stores per pair of
+// MFMAs and global loads per MFMA.  Against the single-region loop with the
+// barrier at the end of the tile: forward -5.5%, dX -8%, dW -2%.
+enum : int { kPipeSpread = 0, kPipeOneSet = 1, kPipeTile = 2 };
+template <int V>
+struct Sched {
+  static constexpr int kPipe = kPipeSpread;
+  static constexpr int kLoadStep = V == kFwd ? 1 : V == kDx ? 0 : 2;
+  static constexpr int kValu = V == kFwd ? 4 : V == kDx ? 2 : 5;
+  static constexpr int kWritesPerPair = 1;
+  static constexpr int kVmemPerMfma = 2;
+};
+
+template <class S, bool VMEM, bool WRITES>
+__device__ __forceinline__ void interleave_kstep() {
+#pragma unroll
+  for (int m = 0; m < 16; ++m) {
+    __builtin_amdgcn_sched_group_barrier(SG_MFMA, 1, 0);
+    if (m < 8) __builtin_amdgcn_sched_group_barrier(SG_DS_READ, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(SG_VALU, S::kValu, 0);
+    if (WRITES && (m & 1)) __builtin_amdgcn_sched_group_barrier(SG_DS_WRITE, S::kWritesPerPair, 0);
+    if (VMEM) __builtin_amdgcn_sched_group_barrier(SG_VMEM_READ, S::kVmemPerMfma, 0);
+  }
+}
+
+// The whole-tile region: the first k-step's fragment reads, then each MFMA
+// followed by a few VALU ops of the next tile's conversion; the following
+// k-steps' reads ride on the first MFMAs of each k-step, the LDS stores of the
+// next tile and the global loads of the tile after it spread over the sequence.
+__device__ __forceinline__ void interleave_tile() {
   __builtin_amdgcn_sched_group_barrier(SG_DS_READ, 8, 0);
 #pragma unroll
   for (int m = 0; m < 64; ++m) {
@@ -499,6 +519,13 @@ __device__ __forceinline__ void interleave() {
     if ((m & 3) == 3) __builtin_amdgcn_sched_group_barrier(SG_DS_WRITE, 1, 0);
     if ((m & 3) == 1) __builtin_amdgcn_sched_group_barrier(SG_VMEM_READ, 1, 0);
   }
+}
+
+// The k-step after the barrier: the next tile's first 8 fragment reads first,
+// then the 16 MFMAs of this tile's last k-step.
+__device__ __forceinline__ void interleave_last() {
+  __builtin_amdgcn_sched_group_barrier(SG_DS_READ, 8, 0);
+  __builtin_amdgcn_sched_group_barrier(SG_MFMA, 16, 0);
 }
 
 // Block -> tile order.  Blocks are dealt round-robin to the 8 XCDs (each with
@@ -541,53 +568,146 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
       #pragma unroll
       for (int v = 0; v < 16; ++v) acc[a][b][v] = 0.f;
 
-  // Two register sets: while the MFMAs consume LDS stage kt%2, the tile
-  // kt+1 held in one set is written to the other stage and the tile kt+2
-  // is fetched into the other set.  Loads past the last tile read zeros or
-  // unused data and are never consumed, so the body has no branches.
+  // Software pipeline over K-tiles of 64.  While the MFMAs consume LDS stage
+  // kt%2, the registers holding tile kt+1 are written to the other stage and
+  // the tile kt+2 is fetched.  kPipe picks the schedule (per GEMM, measured):
+  //  * kPipeSpread: two register sets; the 16 stores of tile kt+1 spread over
+  //    k-steps 0..2 while tile kt+2 loads into the other set from k-step
+  //    kLoadStep on;
+  //  * kPipeOneSet: one register set; the 16 stores in k-step 0, the reload
+  //    with tile kt+2 in k-step 1;
+  //  * kPipeTile: two register sets, the whole tile one scheduling region
+  //    (stores after the MFMAs), the barrier at its end.
+  // In the first two the one barrier per tile sits before k-step 3, whose
+  // fragments are already in registers, so the first fragments of tile kt+1
+  // are read right after it and their latency hides behind k-step 3's MFMAs.
+  // Loads past the last tile read zeros or unused data and are never
+  // consumed, so the body has no branches.
   using Ld = Loader<V, ACT, GRP, VEC, OPT>;
-  Ld L0, L1;
+  using S = Sched<V>;
   const int nk = int((p.K + BK - 1) / BK);
-  L0.load(p, m0, n0, 0);
-  L1.load(p, m0, n0, BK);
-  L0.store(p, lds, lds + 2 * TILE);
-  __syncthreads();
-
-  auto step = [&](int kt, Ld& Lnext, Ld& Lfree) {
-    const uint16_t* As = lds + (kt & 1) * TILE;
-    const uint16_t* Bs = lds + (2 + (kt & 1)) * TILE;
-    const int nx = (kt + 1) & 1;
-    Lfree.load(p, m0, n0, int64_t(kt + 2) * BK);
-    u32x4 fa[2][4], fb[2][4];
-    auto read = [&](u32x4 (&a)[4], u32x4 (&b)[4], int s) {
-      const int ch = 2 * s + (lane >> 5);
+  u32x4 fa[2][4], fb[2][4];
+  auto read = [&](u32x4 (&a)[4], u32x4 (&b)[4], const uint16_t* As, const uint16_t* Bs, int s) {
+    const int ch = 2 * s + (lane >> 5);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) a[i] = *reinterpret_cast<const u32x4*>(As + tile_off(wm + 32 * i + (lane & 31), ch));
+    for (int i = 0; i < 4; ++i) a[i] = *reinterpret_cast<const u32x4*>(As + tile_off(wm + 32 * i + (lane & 31), ch));
 #pragma unroll
-      for (int j = 0; j < 4; ++j) b[j] = *reinterpret_cast<const u32x4*>(Bs + tile_off(wn + 32 * j + (lane & 31), ch));
-    };
-    read(fa[0], fb[0], 0);
-#pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      if (s < 3) read(fa[(s + 1) & 1], fb[(s + 1) & 1], s + 1);
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-          // D = B-tile x A-tile^T: a lane's accumulator holds 4 consecutive output
-          // columns of one output row (8-byte stores; dW: 4 columns of one weight row)
-          acc[i][j] = mfma32(fb[s & 1][j], fa[s & 1][i], acc[i][j]);
-    }
-    Lnext.store(p, lds + nx * TILE, lds + (2 + nx) * TILE);
-    interleave();
-    __syncthreads();
+    for (int j = 0; j < 4; ++j) b[j] = *reinterpret_cast<const u32x4*>(Bs + tile_off(wn + 32 * j + (lane & 31), ch));
   };
-  int kt = 0;
-  for (; kt + 1 < nk; kt += 2) {
-    step(kt, L1, L0);
-    step(kt + 1, L0, L1);
+  auto mfmas = [&](const u32x4 (&a)[4], const u32x4 (&b)[4]) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        // D = B-tile x A-tile^T: a lane's accumulator holds 4 consecutive output
+        // columns of one output row (8-byte stores; dW: 4 columns of one weight row)
+        acc[i][j] = mfma32(b[j], a[i], acc[i][j]);
+  };
+  // order of a tile's 16 LDS stores (A: 0..7, B: 8..15), alternating operands
+  constexpr int kOrder[16] = {0, 8, 1, 9, 2, 10, 3, 11, 4, 12, 5, 13, 6, 14, 7, 15};
+  // the last k-step of tile kt (after the barrier) with the first fragment reads of tile kt+1
+  auto last_kstep = [&](const uint16_t* Asn, const uint16_t* Bsn) {
+    __syncthreads();
+    read(fa[0], fb[0], Asn, Bsn, 0);
+    mfmas(fa[1], fb[1]);
+    interleave_last();
+    __builtin_amdgcn_sched_barrier(0);
+  };
+
+  if constexpr (S::kPipe == kPipeSpread) {
+    Ld L0, L1;
+    L0.load(p, m0, n0, 0);
+    L1.load(p, m0, n0, BK);
+#pragma unroll
+    for (int w = 0; w < 16; ++w) L0.store_one(p, lds, lds + 2 * TILE, w);
+    __syncthreads();
+    read(fa[0], fb[0], lds, lds + 2 * TILE, 0);
+    auto step = [&](int kt, Ld& Lnext, Ld& Lfree) {
+      const uint16_t* As = lds + (kt & 1) * TILE;
+      const uint16_t* Bs = lds + (2 + (kt & 1)) * TILE;
+      uint16_t* Asn = lds + ((kt + 1) & 1) * TILE;
+      uint16_t* Bsn = lds + (2 + ((kt + 1) & 1)) * TILE;
+#pragma unroll
+      for (int s = 0; s < 3; ++s) {
+        if (s == S::kLoadStep) Lfree.load(p, m0, n0, int64_t(kt + 2) * BK);
+        read(fa[(s + 1) & 1], fb[(s + 1) & 1], As, Bs, s + 1);
+        mfmas(fa[s & 1], fb[s & 1]);
+        const int w0 = s == 0 ? 0 : s == 1 ? 6 : 11, w1 = s == 0 ? 6 : s == 1 ? 11 : 16;
+#pragma unroll
+        for (int w = w0; w < w1; ++w) Lnext.store_one(p, Asn, Bsn, kOrder[w]);
+        if (s == S::kLoadStep) interleave_kstep<S, true, true>();
+        else interleave_kstep<S, false, true>();
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      last_kstep(Asn, Bsn);
+    };
+    int kt = 0;
+    for (; kt + 1 < nk; kt += 2) {
+      step(kt, L1, L0);
+      step(kt + 1, L0, L1);
+    }
+    if (kt < nk) step(kt, L1, L0);
+  } else if constexpr (S::kPipe == kPipeOneSet) {
+    Ld L;
+    L.load(p, m0, n0, 0);
+#pragma unroll
+    for (int w = 0; w < 16; ++w) L.store_one(p, lds, lds + 2 * TILE, w);
+    L.load(p, m0, n0, BK);
+    __syncthreads();
+    read(fa[0], fb[0], lds, lds + 2 * TILE, 0);
+    for (int kt = 0; kt < nk; ++kt) {
+      const uint16_t* As = lds + (kt & 1) * TILE;
+      const uint16_t* Bs = lds + (2 + (kt & 1)) * TILE;
+      uint16_t* Asn = lds + ((kt + 1) & 1) * TILE;
+      uint16_t* Bsn = lds + (2 + ((kt + 1) & 1)) * TILE;
+#pragma unroll
+      for (int s = 0; s < 3; ++s) {
+        read(fa[(s + 1) & 1], fb[(s + 1) & 1], As, Bs, s + 1);
+        mfmas(fa[s & 1], fb[s & 1]);
+        if (s == 0) {
+#pragma unroll
+          for (int w = 0; w < 16; ++w) L.store_one(p, Asn, Bsn, kOrder[w]);
+          interleave_kstep<S, false, true>();
+        } else if (s == 1) {
+          L.load(p, m0, n0, int64_t(kt + 2) * BK);
+          interleave_kstep<S, true, false>();
+        } else {
+          interleave_kstep<S, false, false>();
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      last_kstep(Asn, Bsn);
+    }
+  } else {
+    Ld L0, L1;
+    L0.load(p, m0, n0, 0);
+    L1.load(p, m0, n0, BK);
+#pragma unroll
+    for (int w = 0; w < 16; ++w) L0.store_one(p, lds, lds + 2 * TILE, w);
+    __syncthreads();
+    auto step = [&](int kt, Ld& Lnext, Ld& Lfree) {
+      const uint16_t* As = lds + (kt & 1) * TILE;
+      const uint16_t* Bs = lds + (2 + (kt & 1)) * TILE;
+      const int nx = (kt + 1) & 1;
+      Lfree.load(p, m0, n0, int64_t(kt + 2) * BK);
+      read(fa[0], fb[0], As, Bs, 0);
+#pragma unroll
+      for (int s = 0; s < 4; ++s) {
+        if (s < 3) read(fa[(s + 1) & 1], fb[(s + 1) & 1], As, Bs, s + 1);
+        mfmas(fa[s & 1], fb[s & 1]);
+      }
+#pragma unroll
+      for (int w = 0; w < 16; ++w) Lnext.store_one(p, lds + nx * TILE, lds + (2 + nx) * TILE, w);
+      interleave_tile();
+      __syncthreads();
+    };
+    int kt = 0;
+    for (; kt + 1 < nk; kt += 2) {
+      step(kt, L1, L0);
+      step(kt + 1, L0, L1);
+    }
+    if (kt < nk) step(kt, L1, L0);
   }
-  if (kt < nk) step(kt, L1, L0);
 
   // acc[i][j][4g + e] = C[m0 + wm + 32 i + lane % 32][n0 + wn + 32 j + 8 g + 4 (lane / 32) + e]
   if constexpr (V == kFwd || V == kDx) {
