@@ -4,7 +4,9 @@
 
 A step is lrqat_forward followed by lrqat_backward (dX, dA, dB) for every linear
 of the workload, each on its own batch of seeded synthetic inputs already
-resident in device memory.  The default workload is the LLaMA-7B q_proj-shaped
+resident in device memory.  The step is captured once in a HIP graph and
+replayed (each replay checked bit for bit against an eager step); the eager
+rate is reported beside it, and the per-kernel times come from eager steps.  The default workload is the LLaMA-7B q_proj-shaped
 layer 4096 -> 4096 with 8 x 1024 tokens, rank 32, alpha 32, W4 per-channel and
 Phi0 in fixed point Q4.4.  Prints one JSON line.
 
@@ -45,6 +47,7 @@ def parse():
     ap.add_argument("--workload", type=int, default=2)
     ap.add_argument("--rank", type=int, default=0, help="override the workload's rank r (and alpha = r)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--eager", action="store_true", help="time eager launches only (no HIP graph)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU time of the oracle sample")
     ap.add_argument("--vendor-gemm", action="store_true",
                     help="only time the vendor library's plain bf16 GEMMs of the layer's three shapes and exit")
@@ -234,11 +237,18 @@ def main():
     stream = torch.cuda.current_stream()
 
     def step():
+        # on the current stream: the default one, or the capture stream of a HIP graph
         for l in layers:
-            lrqat.lrqat_forward(l["spec"], l["X"], l["phi0"], l["s0"], l["A"], l["B"], Y=l["Y"], ws=ws_f,
-                                stream=stream)
+            lrqat.lrqat_forward(l["spec"], l["X"], l["phi0"], l["s0"], l["A"], l["B"], Y=l["Y"], ws=ws_f)
             lrqat.lrqat_backward(l["spec"], l["X"], l["phi0"], l["s0"], l["A"], l["B"], l["dY"], dX=l["dX"],
-                                 dA=l["dA"], dB=l["dB"], ws=ws_b, stream=stream)
+                                 dA=l["dA"], dB=l["dB"], ws=ws_b)
+
+    def outputs():
+        return [t.clone() for l in layers for t in (l["Y"], l["dX"], l["dA"], l["dB"])]
+
+    def same(a, b):
+        return all(torch.equal(x.view(torch.int16) if x.dtype == torch.bfloat16 else x,
+                               y.view(torch.int16) if y.dtype == torch.bfloat16 else y) for x, y in zip(a, b))
 
     torch.cuda.synchronize()
     torch.cuda.reset_peak_memory_stats(dev)
@@ -246,19 +256,55 @@ def main():
         step()
     torch.cuda.synchronize()
     print(f"[bench] warmup done ({args.warmup} steps)", file=sys.stderr, flush=True)
-    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
-    torch.cuda.synchronize()
-    evs[0].record(stream)
-    for i in range(args.steps):
-        step()
-        evs[i + 1].record(stream)
-    torch.cuda.synchronize()
-    ms = evs[0].elapsed_time(evs[-1]) / args.steps
-    per_step = np.array([evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps)])
+
+    def time_steps(run):
+        evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+        torch.cuda.synchronize()
+        evs[0].record()
+        for i in range(args.steps):
+            run()
+            evs[i + 1].record()
+        torch.cuda.synchronize()
+        return evs[0].elapsed_time(evs[-1]) / args.steps, np.array([evs[i].elapsed_time(evs[i + 1])
+                                                                    for i in range(args.steps)])
+
+    ms_eager, per_step_eager = time_steps(step)
+    print(f"[bench] timed {args.steps} eager steps: {ms_eager:.4f} ms/step", file=sys.stderr, flush=True)
+    # the same step captured once in a HIP graph and replayed; every replay must give the eager step's bits
+    ref = outputs()
+    graph_ok, graph_note = False, "not tried"
+    if not args.eager:
+        try:
+            side = torch.cuda.Stream()
+            side.wait_stream(torch.cuda.current_stream())
+            with torch.cuda.stream(side):
+                step()
+            torch.cuda.current_stream().wait_stream(side)
+            torch.cuda.synchronize()
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                step()
+            graph_ok = True
+            for _ in range(3):
+                for l in layers:
+                    for key in ("Y", "dX", "dA", "dB"):
+                        l[key].fill_(float("nan"))
+                g.replay()
+                torch.cuda.synchronize()
+                graph_ok = graph_ok and same(outputs(), ref)
+                step()  # eager work between replays
+                torch.cuda.synchronize()
+            graph_note = "replays bit-identical to the eager step" if graph_ok else "replay differs: eager timing used"
+        except Exception as e:  # pragma: no cover - capture unsupported
+            graph_ok, graph_note = False, f"capture failed: {type(e).__name__}: {e}"
+    if graph_ok:
+        ms, per_step = time_steps(g.replay)
+        print(f"[bench] timed {args.steps} graph replays: {ms:.4f} ms/step", file=sys.stderr, flush=True)
+    else:
+        ms, per_step = ms_eager, per_step_eager
     peak_mem = torch.cuda.max_memory_allocated(dev)
     flops = wl.flops_fwd_bwd()
     value = flops / (ms * 1e-3) / 1e12
-    print(f"[bench] timed {args.steps} steps: {ms:.4f} ms/step", file=sys.stderr, flush=True)
 
     # per-kernel durations (HIP events around each launch on the library's stream)
     lrqat.lrqat_timing_reset()
@@ -345,6 +391,8 @@ def main():
                    "alpha": wl.alpha, "bits": wl.bits, "phi_format": wl.phi_format, "group_size": wl.group_size,
                    "act_bits": wl.act_bits, "parallelism": "none"},
         "step_ms_p10_p50_p90": [float(np.percentile(per_step, q)) for q in (10, 50, 90)],
+        "launch": "hip_graph" if graph_ok else "eager", "hip_graph": graph_note,
+        "ms_per_step_eager": ms_eager,
         "pct_of_bf16_peak": 100.0 * value / PEAK_BF16_TFLOPS,
         "tokens_per_s": T / (ms * 1e-3),
         "peak_device_mem_bytes": int(peak_mem),

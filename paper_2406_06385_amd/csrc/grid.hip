@@ -266,7 +266,8 @@ __device__ __forceinline__ uint32_t pack_nibble_bytes(uint32_t q0, uint32_t q1) 
 }
 
 // Rounding decision, clip, packing and mask of one 16 x 64 wave tile, by the
-// cheapest of three paths that is exact for the whole wave:
+// cheapest of the paths that is exact for the whole wave (INT-b Phi0 whose
+// |delta| bound is below 1/2 on the whole tile has been copied already):
 //  * delta identically zero on the strip (B = 0, the adapters' initial
 //    state): round-half-even of Phi0, decided in integers;
 //  * byte-parallel (swar_grid_q8): every |delta| is below the distance of the
@@ -281,7 +282,7 @@ __device__ __forceinline__ uint32_t pack_nibble_bytes(uint32_t q0, uint32_t q1) 
 //    margins and float64 deltas (rare).
 template <bool PACKED, bool MASK, bool B4, bool Q8OUT>
 __device__ __forceinline__ void grid_finish(const GridArgs& a, const PhiRegs& P, const f32x4 (&acc)[4], float tau,
-                                            bool zero_delta, int64_t row, int64_t c16) {
+                                            bool zero_delta, int64_t row, int64_t c16, bool small_delta = false) {
   const int bits = B4 ? 4 : a.bits;  // B4: the common 4-bit grid, constant for the compiler
   const int lo = -(1 << (bits - 1)), hi = (1 << (bits - 1)) - 1;
   const int f = PACKED ? 0 : 8 - bits;
@@ -294,7 +295,15 @@ __device__ __forceinline__ void grid_finish(const GridArgs& a, const PhiRegs& P,
   uint32_t qb[4] = {0, 0, 0, 0};  // 16 bytes (q as int8, Q8OUT)
   uint32_t mb = 0;            // clip-mask bits of the lane's 16 columns
   bool done = false;  // q words (and an all-ones mask) already formed by the byte-parallel path
-  if (!zero_delta) {
+  if constexpr (PACKED) {
+    if (small_delta) {  // the wave tile's |delta| is provably below 1/2: q is Phi0
+      w0 = P.w[0];
+      w1 = P.w[1];
+      mb = 0xFFFFu;
+      done = true;
+    }
+  }
+  if (!done && !zero_delta) {
     // the regime of the byte-parallel path: every |delta| below the distance of the non-tie
     // codes to their rounding points and above the error bound (so its sign is certain)
     const float tz = fmaxf(tau, 0.f);
@@ -620,13 +629,30 @@ __global__ __launch_bounds__(GR_THREADS) void k_grid(GridArgs a) {
         if constexpr (COAL) load_a_coal(rowblk + 1);
         else load_a(xa, a, rowblk + 1, 0, avec);
       }
-      u32x4 ah, al;
-      split8(x, ah, al);
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         ass = __builtin_fmaf(x[e], x[e], ass);
         amx = fmaxf(amx, fabsf(x[e]));
       }
+      // row norm: the 4 lanes l % 16 + 16 g hold the 4 rank slices of the row
+      ass += __shfl_xor(ass, 16);
+      ass += __shfl_xor(ass, 32);
+      amx = fmaxf(amx, __shfl_xor(amx, 16));
+      amx = fmaxf(amx, __shfl_xor(amx, 32));
+      bool small = false;
+      if constexpr (PACKED) {
+        // integer Phi0: |delta| <= |c| ||A_i|| ||B_j|| below 1/2 on the whole wave tile means
+        // q = Phi0 (no rounding can move, nothing clips), decided without the product
+        const float bound = fabsf(a.c) * norm_bound(ass, amx, a.r) * nb * 1.02f;
+        // (4-bit grids only: a narrower grid may clip an INT4 code of Phi0)
+        small = (B4 || a.bits == 4) && !__builtin_amdgcn_ballot_w64(!(bound < 0.5f - 0x1p-20f));
+      }
+      if (small) {
+        grid_finish<PACKED, MASK, B4, Q8OUT>(a, Pc, acc, 0.f, false, row, c16, true);
+        continue;
+      }
+      u32x4 ah, al;
+      split8(x, ah, al);
 #pragma unroll
       for (int cb = 0; cb < 4; ++cb) {
         const u32x4 ph = bfrag[wave][0][cb][lane], pl = bfrag[wave][1][cb][lane];
@@ -657,12 +683,12 @@ __global__ __launch_bounds__(GR_THREADS) void k_grid(GridArgs a) {
           acc[cb] = mfma16(ph, al, acc[cb]);
         }
       }
+      // row norm: the 4 lanes l % 16 + 16 g hold the 4 rank slices of the row
+      ass += __shfl_xor(ass, 16);
+      ass += __shfl_xor(ass, 32);
+      amx = fmaxf(amx, __shfl_xor(amx, 16));
+      amx = fmaxf(amx, __shfl_xor(amx, 32));
     }
-    // row norm: the 4 lanes l % 16 + 16 g hold the 4 rank slices of the row
-    ass += __shfl_xor(ass, 16);
-    ass += __shfl_xor(ass, 32);
-    amx = fmaxf(amx, __shfl_xor(amx, 16));
-    amx = fmaxf(amx, __shfl_xor(amx, 32));
     // -1 where delta is exactly zero (a zero A row or zero B columns, e.g. B at its zero
     // initialisation), so that no element is re-decided there
     const float tau = amx == 0.f ? -1.f : a.tau_coef * norm_bound(ass, amx, a.r) * nb;
