@@ -127,7 +127,7 @@ __global__ __launch_bounds__(256) void k_encode(const float* __restrict__ W0, co
 // near n = 0 it is exact.  Elements inside that bound are decided again from
 // a float64 delta, so the grid equals the exact one except within float64
 // rounding of a .5 point.
-constexpr int GR_COLS = 64, GR_THREADS = 256, GR_MIN_BLOCKS = 512;
+constexpr int GR_COLS = 64, GR_THREADS = 256, GR_MIN_BLOCKS = 512, GRW_MIN_BLOCKS = 1024;
 
 // 16x16x32 MFMA, D(16x16, f32) += P(16x32, bf16) Q(32x16, bf16): lane l
 // supplies row l % 16 of P and column l % 16 of Q, each with the 8 K-values
@@ -280,9 +280,18 @@ __device__ __forceinline__ uint32_t pack_nibble_bytes(uint32_t q0, uint32_t q1) 
 //    n + [w > 0].  That is certain unless |w| lies within tau of 0 or is at
 //    least 1 - tau; a wave with such an element redoes its tile with exact
 //    margins and float64 deltas (rare).
+// The lane's results for its 16 columns: q as 16 nibbles (w0, w1) or 16 bytes
+// (qb, Q8OUT), and the clip-mask bits.
+struct GridOut {
+  uint32_t w0, w1;
+  uint32_t qb[4];
+  uint32_t mb;
+};
+
 template <bool PACKED, bool MASK, bool B4, bool Q8OUT>
-__device__ __forceinline__ void grid_finish(const GridArgs& a, const PhiRegs& P, const f32x4 (&acc)[4], float tau,
-                                            bool zero_delta, int64_t row, int64_t c16, bool small_delta = false) {
+__device__ __forceinline__ void grid_decide(const GridArgs& a, const PhiRegs& P, const f32x4 (&acc)[4], float tau,
+                                            bool zero_delta, int64_t row, int64_t c16, bool small_delta,
+                                            GridOut& o) {
   const int bits = B4 ? 4 : a.bits;  // B4: the common 4-bit grid, constant for the compiler
   const int lo = -(1 << (bits - 1)), hi = (1 << (bits - 1)) - 1;
   const int f = PACKED ? 0 : 8 - bits;
@@ -462,7 +471,21 @@ __device__ __forceinline__ void grid_finish(const GridArgs& a, const PhiRegs& P,
       w1 &= uint32_t(keep >> 32);
     }
   }
-  if (row_ok && c16 < a.kq) {
+  o.w0 = w0;
+  o.w1 = w1;
+#pragma unroll
+  for (int g = 0; g < 4; ++g) o.qb[g] = qb[g];
+  o.mb = mb;
+}
+
+// Stores one lane's 16 columns of q (and mask) at row, columns c16 .. c16 + 15.
+template <bool MASK, bool Q8OUT>
+__device__ __forceinline__ void grid_store(const GridArgs& a, const GridOut& o, int64_t row, int64_t c16) {
+  const uint32_t w0 = o.w0, w1 = o.w1, mb = o.mb;
+  uint32_t qb[4];
+#pragma unroll
+  for (int g = 0; g < 4; ++g) qb[g] = o.qb[g];
+  if (row < a.m && c16 < a.kq) {
     if constexpr (Q8OUT) {
       uint8_t* dst = a.qout + row * a.ldq + c16;
       if (c16 + 16 <= a.kq && (reinterpret_cast<uintptr_t>(dst) & 15) == 0) {
@@ -482,6 +505,14 @@ __device__ __forceinline__ void grid_finish(const GridArgs& a, const PhiRegs& P,
     }
     if constexpr (MASK) a.mout[row * a.ldm + (c16 >> 4)] = uint16_t(mb);
   }
+}
+
+template <bool PACKED, bool MASK, bool B4, bool Q8OUT>
+__device__ __forceinline__ void grid_finish(const GridArgs& a, const PhiRegs& P, const f32x4 (&acc)[4], float tau,
+                                            bool zero_delta, int64_t row, int64_t c16, bool small_delta = false) {
+  GridOut o;
+  grid_decide<PACKED, MASK, B4, Q8OUT>(a, P, acc, tau, zero_delta, row, c16, small_delta, o);
+  grid_store<MASK, Q8OUT>(a, o, row, c16);
 }
 
 // COAL (r = 32, 16-byte aligned A and B rows, k % 4 == 0): B and A are read
@@ -696,6 +727,241 @@ __global__ __launch_bounds__(GR_THREADS) void k_grid(GridArgs a) {
   }
 }
 
+// Wide tiles, for r = 32 with 16-byte aligned A and B rows, k % 4 == 0 and
+// 16-byte aligned Phi0 rows.
+// A block owns 256 adjacent columns (a strip) and 4 nit consecutive 16-row
+// blocks; wave w takes row blocks 4 it + w across the whole strip, so that one
+// 16-row A slice serves 4096 outputs.  The strip is computed as four
+// sub-tiles of 16 x 64 (sixteen 16x16 MFMA tiles) whose B columns are
+// assigned so that lane l owns 64 consecutive columns, 64 (l / 16) .. +63,
+// of weight row l % 16: in sub-tile j, MFMA row i of column block cb stands
+// for strip column 64 (i / 4) + 16 j + 4 cb + i % 4.  A lane's Phi0 codes,
+// q nibbles and mask words of the strip are then 32 (64) contiguous bytes,
+// moved with 16-byte accesses that cover whole 128-byte lines per row.  Wave w
+// builds the B fragments of sub-tile w in LDS; all four waves read all four.
+// Blocks are numbered so that each XCD (blocks are dispatched round-robin
+// over the 8 XCDs) takes a contiguous range of row blocks, keeping the A rows
+// in one L2.  The decision per sub-tile is grid_decide, as in k_grid.
+template <bool PACKED>
+__device__ __forceinline__ void load_phi_w(PhiRegs (&P)[4], const GridArgs& a, int64_t rowblk, int64_t strip0) {
+  const int lane = threadIdx.x & 63, g = lane >> 4;
+  const int64_t row0 = rowblk * 16, cb0 = PACKED ? strip0 / 2 : strip0;
+  const auto r = grid_rsrc(a.phi0 + row0 * a.ld_phi + cb0, (a.m - row0) * a.ld_phi - cb0);
+  // the lane's bytes: 32 g .. +31 (packed) or 64 g .. +63 (Q8) of the row's strip
+  const uint32_t off = uint32_t((lane & 15) * a.ld_phi + (PACKED ? 32 : 64) * g);
+#pragma unroll
+  for (int h = 0; h < (PACKED ? 2 : 4); ++h) {
+    const u32x4 v = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, int(off + 16 * h), 0, 0));
+    if constexpr (PACKED) {
+      P[2 * h] = PhiRegs{{v[0], v[1], 0u, 0u}};
+      P[2 * h + 1] = PhiRegs{{v[2], v[3], 0u, 0u}};
+    } else {
+      P[h] = PhiRegs{{v[0], v[1], v[2], v[3]}};
+    }
+  }
+}
+
+template <bool PACKED, bool MASK, bool B4, bool Q8OUT>
+__global__ __launch_bounds__(GR_THREADS) void k_grid_w(GridArgs a) {
+  const int lane = threadIdx.x & 63, g = lane >> 4;
+  const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x >> 6));
+  // logical block: XCD x = blockIdx % 8 takes the contiguous range starting at x floor(N/8) + min(x, N % 8)
+  const int64_t nblk = gridDim.x, x = blockIdx.x % 8;
+  const int64_t lb = x * (nblk / 8) + min<int64_t>(x, nblk % 8) + blockIdx.x / 8;
+  const int64_t nstrips = (a.kq + 4 * GR_COLS - 1) / (4 * GR_COLS);
+  const int64_t strip0 = (lb % nstrips) * 4 * GR_COLS;
+  const int64_t rb0 = (lb / nstrips) * 4 * a.nit + wave;  // the wave's first 16-row block
+
+  __shared__ __attribute__((aligned(16))) u32x4 bfrag[4][2][4][64];
+  __shared__ __attribute__((aligned(16))) float arow[4][16][36];  // the wave's A rows (144-byte pitch)
+  __shared__ float nbs[4];                                         // column-norm bound per sub-tile
+
+  // round 0's codes and A rows first: they do not depend on the B fragments
+  PhiRegs P[4];
+  u32x4 xc[2];  // the 16 A rows of a round: rows lane / 8 and 8 + lane / 8, 16-byte chunk lane % 8
+  auto load_round = [&](int64_t rblk) {
+    load_phi_w<PACKED>(P, a, rblk, strip0);
+    const auto r = grid_rsrc(a.A + rblk * 16 * 32, (a.m - rblk * 16) * 128);
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+      xc[h] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, 1024 * h + 16 * lane, 0, 0));
+  };
+  load_round(rb0);
+
+  {
+    // B[0..31] at the strip columns 64 q + 16 w + c (q = 0..3, c = 0..15) of sub-tile w:
+    // 8 loads of 4 rank rows, staged raw (rank row-major, 64 floats, position 16 q + c)
+    // in the wave's fragment region, then read back in operand order
+    float* raw = reinterpret_cast<float*>(&bfrag[wave][0][0][0]);
+    const auto rb = grid_rsrc(a.B + strip0, int64_t(a.r) * a.k * 4 - strip0 * 4);
+    const int cl = 4 * (lane & 15);                                             // raw position
+    const int64_t gc = 64 * ((lane & 15) >> 2) + 16 * wave + 4 * (lane & 3);  // strip column
+    u32x4 v[8];
+#pragma unroll
+    for (int t = 0; t < 8; ++t)
+      v[t] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                                           rb, int(uint32_t(((4 * t + (lane >> 4)) * a.k + gc) * 4)), 0, 0));
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) v[t][j] = strip0 + gc + j < a.k ? v[t][j] : 0u;
+      *reinterpret_cast<u32x4*>(raw + (4 * t + (lane >> 4)) * 64 + cl) = v[t];
+    }
+    float y[4][8];
+    float ss[4] = {0.f, 0.f, 0.f, 0.f}, bss = 0.f, bmx = 0.f;
+#pragma unroll
+    for (int cb = 0; cb < 4; ++cb)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        y[cb][e] = raw[(8 * (lane >> 4) + e) * 64 + 16 * ((lane & 15) >> 2) + 4 * cb + (lane & 3)];
+        ss[cb] = __builtin_fmaf(y[cb][e], y[cb][e], ss[cb]);
+        bmx = fmaxf(bmx, fabsf(y[cb][e]));
+      }
+#pragma unroll
+    for (int cb = 0; cb < 4; ++cb) {
+      u32x4 h, l;
+      split8(y[cb], h, l);
+      bfrag[wave][0][cb][lane] = h;
+      bfrag[wave][1][cb][lane] = l;
+      ss[cb] += __shfl_xor(ss[cb], 16);
+      ss[cb] += __shfl_xor(ss[cb], 32);
+      bss = fmaxf(bss, ss[cb]);
+    }
+    for (int off = 1; off < 64; off <<= 1) {
+      bss = fmaxf(bss, __shfl_xor(bss, off));
+      bmx = fmaxf(bmx, __shfl_xor(bmx, off));
+    }
+    // 0 exactly when the sub-tile's B columns are all zero
+    if (lane == 0) nbs[wave] = norm_bound(bss, bmx, a.r);
+  }
+  __syncthreads();
+  float nbv[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) nbv[j] = nbs[j];
+  const int64_t cl0_ = strip0 + 64 * g;  // the lane's first column
+
+  int64_t rowblk = rb0;
+  for (int it = 0; it < a.nit; ++it, rowblk += 4) {
+    if (rowblk * 16 >= a.m) break;  // wave-uniform
+    const int64_t row = rowblk * 16 + (lane & 15);
+    // opaque per round, like the sub-tile index below: bounds and addresses derived
+    // from the lane's columns are formed where they are used, not kept across rounds
+    int64_t cl0 = cl0_;
+    asm volatile("" : "+v"(cl0));
+    // through the wave's LDS rows: lane l takes row l % 16, ranks 8 (l / 16) .. +7
+#pragma unroll
+    for (int h = 0; h < 2; ++h) *reinterpret_cast<u32x4*>(&arow[wave][8 * h + (lane >> 3)][4 * (lane & 7)]) = xc[h];
+    float x[8];
+    {
+      const f32x4 u = *reinterpret_cast<const f32x4*>(&arow[wave][lane & 15][8 * (lane >> 4)]);
+      const f32x4 w = *reinterpret_cast<const f32x4*>(&arow[wave][lane & 15][8 * (lane >> 4) + 4]);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        x[e] = u[e];
+        x[4 + e] = w[e];
+      }
+    }
+    PhiRegs Pc[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) Pc[j] = P[j];
+    if (it + 1 < a.nit) load_round(rowblk + 4);
+    float ass = 0.f, amx = 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      ass = __builtin_fmaf(x[e], x[e], ass);
+      amx = fmaxf(amx, fabsf(x[e]));
+    }
+    // row norm: the 4 lanes l % 16 + 16 g hold the 4 rank slices of the row
+    ass += __shfl_xor(ass, 16);
+    ass += __shfl_xor(ass, 32);
+    amx = fmaxf(amx, __shfl_xor(amx, 16));
+    amx = fmaxf(amx, __shfl_xor(amx, 32));
+    const float na = norm_bound(ass, amx, a.r);
+    u32x4 ah, al;
+    split8(x, ah, al);
+    GridOut out[4];
+#pragma unroll 1
+    for (int jl = 0; jl < 4; ++jl) {
+      // opaque copy of the sub-tile index: keeps the compiler from hoisting per-sub-tile
+      // addresses and bounds of all four sub-tiles out of the round loop into registers
+      int j = jl;
+      asm volatile("" : "+s"(j));
+      PhiRegs Pj = Pc[0];
+      float nb = nbv[0];
+#pragma unroll
+      for (int t = 1; t < 4; ++t)
+        if (j == t) {
+          nb = nbv[t];
+          Pj = Pc[t];
+        }
+      const int64_t c16 = cl0 + 16 * j;
+      f32x4 acc[4];
+#pragma unroll
+      for (int cb = 0; cb < 4; ++cb) acc[cb] = f32x4{0.f, 0.f, 0.f, 0.f};
+      GridOut o;
+      bool small = false;
+      if constexpr (PACKED) {
+        // integer Phi0: |delta| <= |c| ||A_i|| ||B_j|| below 1/2 on the whole sub-tile means
+        // q = Phi0 (no rounding can move, nothing clips on a 4-bit grid)
+        const float bound = fabsf(a.c) * na * nb * 1.02f;
+        small = (B4 || a.bits == 4) && !__builtin_amdgcn_ballot_w64(!(bound < 0.5f - 0x1p-20f));
+      }
+      if (small) {
+        grid_decide<PACKED, MASK, B4, Q8OUT>(a, Pj, acc, 0.f, false, row, c16, true, o);
+      } else {
+#pragma unroll
+        for (int cb = 0; cb < 4; ++cb) {
+          const u32x4 ph = bfrag[j][0][cb][lane], pl = bfrag[j][1][cb][lane];
+          acc[cb] = mfma16(ph, ah, acc[cb]);
+          acc[cb] = mfma16(pl, ah, acc[cb]);
+          acc[cb] = mfma16(ph, al, acc[cb]);
+        }
+        // -1 where delta is exactly zero (a zero A row), so that no element is re-decided there
+        const float tau = amx == 0.f ? -1.f : a.tau_coef * na * nb;
+        grid_decide<PACKED, MASK, B4, Q8OUT>(a, Pj, acc, tau, nb == 0.f, row, c16, false, o);
+      }
+#pragma unroll
+      for (int t = 0; t < 4; ++t)
+        if (j == t) out[t] = o;
+    }
+    // stores: the lane's 64 columns at once where they lie inside kq and are aligned
+    const bool whole = row < a.m && cl0 + 64 <= a.kq;
+    if constexpr (Q8OUT) {
+      uint8_t* dst = a.qout + row * a.ldq + cl0;
+      if (whole && (reinterpret_cast<uintptr_t>(dst) & 15) == 0) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          *reinterpret_cast<u32x4*>(dst + 16 * j) = u32x4{out[j].qb[0], out[j].qb[1], out[j].qb[2], out[j].qb[3]};
+      } else {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) grid_store<false, true>(a, out[j], row, cl0 + 16 * j);
+      }
+    } else {
+      uint8_t* dst = a.qout + row * a.ldq + (cl0 >> 1);
+      if (whole && (reinterpret_cast<uintptr_t>(dst) & 15) == 0) {
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+          *reinterpret_cast<u32x4*>(dst + 16 * h) =
+              u32x4{out[2 * h].w0, out[2 * h].w1, out[2 * h + 1].w0, out[2 * h + 1].w1};
+      } else {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) grid_store<false, false>(a, out[j], row, cl0 + 16 * j);
+      }
+    }
+    if constexpr (MASK) {
+      uint16_t* md = a.mout + row * a.ldm + (cl0 >> 4);
+      if (whole && (reinterpret_cast<uintptr_t>(md) & 7) == 0) {
+        *reinterpret_cast<u32x2*>(md) =
+            u32x2{(out[0].mb & 0xFFFFu) | (out[1].mb << 16), (out[2].mb & 0xFFFFu) | (out[3].mb << 16)};
+      } else if (row < a.m) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          if (cl0 + 16 * j < a.kq) md[j] = uint16_t(out[j].mb);
+      }
+    }
+  }
+}
+
 // ============================================================================ activations
 // One block per token row: s_x = max|X_t| / 127, n = clip(round(X_t / s_x), -128, 127).
 // Outputs (each optional): the codes n [T][ldn] (columns k..ldn-1 written as
@@ -793,6 +1059,39 @@ hipError_t launch_grid(const GridArgs& a0, hipStream_t st) {
   // 4-bit grids (the common W4 case) get an instantiation with the width fixed
   const int sel = (a.packed ? 8 : 0) | (a.r <= 32 ? 4 : 0) | (coal ? 2 : 0) | (a.mout ? 1 : 0);
   const bool b4 = a.bits == 4;
+  // wide tiles where they still give GRW_MIN_BLOCKS blocks: rounds of 64 rows per block,
+  // the most (up to 4) that keep that many
+  const int64_t nrb64 = (a.m + 63) / 64;
+  const bool phi16 = ((a.ld_phi | int64_t(reinterpret_cast<uintptr_t>(a.phi0))) & 15) == 0;
+  if (coal && phi16 && nstrips * nrb64 >= GRW_MIN_BLOCKS) {
+    GridArgs w = a;
+    w.nit = 4;
+    while (w.nit > 1 && nstrips * ((nrb64 + w.nit - 1) / w.nit) < GRW_MIN_BLOCKS) w.nit /= 2;
+    const unsigned nbw = unsigned(nstrips * ((nrb64 + w.nit - 1) / w.nit));
+    const int wsel = (a.packed ? 4 : 0) | (a.mout ? 2 : 0) | (b4 ? 1 : 0);
+    if (a.q8out) {
+      if (a.packed || a.bits <= 4) return hipErrorInvalidValue;
+      if (a.mout) k_grid_w<false, true, false, true><<<nbw, GR_THREADS, 0, st>>>(w);
+      else k_grid_w<false, false, false, true><<<nbw, GR_THREADS, 0, st>>>(w);
+      return hipGetLastError();
+    }
+    switch (wsel) {
+#define LRQAT_GRIDW_CASE(S, P, M, B)                                        \
+  case S:                                                                   \
+    k_grid_w<P, M, B, false><<<nbw, GR_THREADS, 0, st>>>(w);                \
+    break;
+      LRQAT_GRIDW_CASE(0, false, false, false)
+      LRQAT_GRIDW_CASE(1, false, false, true)
+      LRQAT_GRIDW_CASE(2, false, true, false)
+      LRQAT_GRIDW_CASE(3, false, true, true)
+      LRQAT_GRIDW_CASE(4, true, false, false)
+      LRQAT_GRIDW_CASE(5, true, false, true)
+      LRQAT_GRIDW_CASE(6, true, true, false)
+      LRQAT_GRIDW_CASE(7, true, true, true)
+#undef LRQAT_GRIDW_CASE
+    }
+    return hipGetLastError();
+  }
   // grids wider than 4 bits (fixed point b = 5..7) are written as int8
   if (a.q8out) {
     if (a.packed || a.bits <= 4) return hipErrorInvalidValue;
