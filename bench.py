@@ -43,7 +43,7 @@ def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=100)
     ap.add_argument("--workload", type=int, default=2)
     ap.add_argument("--rank", type=int, default=0, help="override the workload's rank r (and alpha = r)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -269,6 +269,8 @@ def main():
                                                                     for i in range(args.steps)])
 
     ms_eager, per_step_eager = time_steps(step)
+    # device memory of the training steps themselves (before the graph-check copies below)
+    peak_mem_steps = torch.cuda.max_memory_allocated(dev)
     print(f"[bench] timed {args.steps} eager steps: {ms_eager:.4f} ms/step", file=sys.stderr, flush=True)
     # the same step captured once in a HIP graph and replayed; every replay must give the eager step's bits
     ref = outputs()
@@ -326,6 +328,21 @@ def main():
     roofline = {"kernel": dom, "bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                 "frac": achieved / PEAK_BF16_TFLOPS if achieved else None, "traffic": traffic,
                 "avg_launch_us": 1e3 * per[dom][1] / per[dom][0], "launches_per_step": per[dom][0] // args.steps}
+
+    # the integer-grid pass against HBM: algorithmic bytes of one launch (codes in, q out, A and B,
+    # plus the clip mask in the backward's launches), averaged over the step's forward and backward launches
+    grid_pass = None
+    if "grid" in per:
+        def grid_bytes(l, mask):
+            L = l["spec"]
+            b = l["phi0"].numel() * l["phi0"].element_size() + 4 * (L.out_features + L.in_features) * r
+            b += L.out_features * L.in_features // (2 if wl.bits <= 4 else 1)
+            return b + (L.out_features * L.in_features // 8 if mask else 0)
+        gb = sum(grid_bytes(l, False) + grid_bytes(l, True) for l in layers) / (2 * nl)
+        g_us = 1e3 * per["grid"][1] / per["grid"][0]
+        grid_pass = {"bound": "hbm", "achieved": gb / (g_us * 1e-6) / 1e9, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": gb / (g_us * 1e-6) / 1e9 / PEAK_HBM_GBS, "bytes_per_launch": gb, "avg_launch_us": g_us,
+                     "traffic": traffic_record("grid") if nl == 1 else None}
 
     # merge of every layer (W_Z for inference) and a plain device copy, as bandwidth
     merge_bytes = sum(l["phi0"].numel() * l["phi0"].element_size() + 4 * (l["spec"].out_features +
@@ -413,11 +430,13 @@ def main():
         "ms_per_step_eager": ms_eager,
         "pct_of_bf16_peak": 100.0 * value / PEAK_BF16_TFLOPS,
         "tokens_per_s": T / (ms * 1e-3),
-        "peak_device_mem_bytes": int(peak_mem),
+        "peak_device_mem_bytes": int(peak_mem_steps),
+        "peak_device_mem_bytes_process": int(peak_mem),
         "analytic_mem_bytes": {**analytic, "total": int(sum(analytic.values()))},
         "merge": merge,
         "kernels": kernels,
         "roofline": roofline,
+        "grid_pass": grid_pass,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)

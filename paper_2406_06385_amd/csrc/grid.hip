@@ -127,7 +127,10 @@ __global__ __launch_bounds__(256) void k_encode(const float* __restrict__ W0, co
 // near n = 0 it is exact.  Elements inside that bound are decided again from
 // a float64 delta, so the grid equals the exact one except within float64
 // rounding of a .5 point.
-constexpr int GR_COLS = 64, GR_THREADS = 256, GR_MIN_BLOCKS = 512, GRW_MIN_BLOCKS = 1024;
+#ifndef LRQAT_GRW_MIN_BLOCKS
+#define LRQAT_GRW_MIN_BLOCKS 512
+#endif
+constexpr int GR_COLS = 64, GR_THREADS = 256, GR_MIN_BLOCKS = 512, GRW_MIN_BLOCKS = LRQAT_GRW_MIN_BLOCKS;
 
 // 16x16x32 MFMA, D(16x16, f32) += P(16x32, bf16) Q(32x16, bf16): lane l
 // supplies row l % 16 of P and column l % 16 of Q, each with the 8 K-values
@@ -761,7 +764,7 @@ __device__ __forceinline__ void load_phi_w(PhiRegs (&P)[4], const GridArgs& a, i
   }
 }
 
-template <bool PACKED, bool MASK, bool B4, bool Q8OUT>
+template <bool PACKED, bool MASK, bool B4, bool Q8OUT, bool MULTI>
 __global__ __launch_bounds__(GR_THREADS) void k_grid_w(GridArgs a) {
   const int lane = threadIdx.x & 63, g = lane >> 4;
   const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x >> 6));
@@ -771,6 +774,7 @@ __global__ __launch_bounds__(GR_THREADS) void k_grid_w(GridArgs a) {
   const int64_t nstrips = (a.kq + 4 * GR_COLS - 1) / (4 * GR_COLS);
   const int64_t strip0 = (lb % nstrips) * 4 * GR_COLS;
   const int64_t rb0 = (lb / nstrips) * 4 * a.nit + wave;  // the wave's first 16-row block
+  const int nks = MULTI ? a.r / 32 : 1;                       // 32-rank chunks (MULTI: r a multiple of 32)
 
   __shared__ __attribute__((aligned(16))) u32x4 bfrag[4][2][4][64];
   __shared__ __attribute__((aligned(16))) float arow[4][16][36];  // the wave's A rows (144-byte pitch)
@@ -778,20 +782,27 @@ __global__ __launch_bounds__(GR_THREADS) void k_grid_w(GridArgs a) {
 
   // round 0's codes and A rows first: they do not depend on the B fragments
   PhiRegs P[4];
-  u32x4 xc[2];  // the 16 A rows of a round: rows lane / 8 and 8 + lane / 8, 16-byte chunk lane % 8
-  auto load_round = [&](int64_t rblk) {
-    load_phi_w<PACKED>(P, a, rblk, strip0);
-    const auto r = grid_rsrc(a.A + rblk * 16 * 32, (a.m - rblk * 16) * 128);
+  u32x4 xc[2];  // 16 A rows x 32 ranks of a round: rows lane / 8 and 8 + lane / 8, 16-byte chunk lane % 8
+  auto load_a_chunk = [&](int64_t rblk, int ch) {
+    const auto r = grid_rsrc(a.A + rblk * 16 * a.r, (a.m - rblk * 16) * int64_t(a.r) * 4);
 #pragma unroll
     for (int h = 0; h < 2; ++h)
-      xc[h] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, 1024 * h + 16 * lane, 0, 0));
+      xc[h] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                                            r, int(uint32_t((8 * h + (lane >> 3)) * a.r * 4 + 128 * ch + 16 * (lane & 7))),
+                                            0, 0));
+  };
+  auto load_round = [&](int64_t rblk) {
+    load_phi_w<PACKED>(P, a, rblk, strip0);
+    load_a_chunk(rblk, 0);
   };
   load_round(rb0);
 
-  {
-    // B[0..31] at the strip columns 64 q + 16 w + c (q = 0..3, c = 0..15) of sub-tile w:
-    // 8 loads of 4 rank rows, staged raw (rank row-major, 64 floats, position 16 q + c)
-    // in the wave's fragment region, then read back in operand order
+  // B[32 ch .. 32 ch + 31] at the strip columns 64 q + 16 w + c (q = 0..3, c = 0..15) of
+  // sub-tile w: 8 loads of 4 rank rows, staged raw (rank row-major, 64 floats, position
+  // 16 q + c) in the wave's fragment region, then read back in operand order.  ssc[cb]
+  // accumulates the squared norm of the lane's column of block cb, bmx the largest |B|.
+  float ssc[4] = {0.f, 0.f, 0.f, 0.f}, bmx = 0.f;
+  auto stage_b = [&](int ch) {
     float* raw = reinterpret_cast<float*>(&bfrag[wave][0][0][0]);
     const auto rb = grid_rsrc(a.B + strip0, int64_t(a.r) * a.k * 4 - strip0 * 4);
     const int cl = 4 * (lane & 15);                                             // raw position
@@ -800,7 +811,7 @@ __global__ __launch_bounds__(GR_THREADS) void k_grid_w(GridArgs a) {
 #pragma unroll
     for (int t = 0; t < 8; ++t)
       v[t] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
-                                           rb, int(uint32_t(((4 * t + (lane >> 4)) * a.k + gc) * 4)), 0, 0));
+                                           rb, int(uint32_t(((32 * ch + 4 * t + (lane >> 4)) * a.k + gc) * 4)), 0, 0));
 #pragma unroll
     for (int t = 0; t < 8; ++t) {
 #pragma unroll
@@ -808,7 +819,7 @@ __global__ __launch_bounds__(GR_THREADS) void k_grid_w(GridArgs a) {
       *reinterpret_cast<u32x4*>(raw + (4 * t + (lane >> 4)) * 64 + cl) = v[t];
     }
     float y[4][8];
-    float ss[4] = {0.f, 0.f, 0.f, 0.f}, bss = 0.f, bmx = 0.f;
+    float ss[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int cb = 0; cb < 4; ++cb)
 #pragma unroll
@@ -825,60 +836,115 @@ __global__ __launch_bounds__(GR_THREADS) void k_grid_w(GridArgs a) {
       bfrag[wave][1][cb][lane] = l;
       ss[cb] += __shfl_xor(ss[cb], 16);
       ss[cb] += __shfl_xor(ss[cb], 32);
-      bss = fmaxf(bss, ss[cb]);
+      ssc[cb] += ss[cb];
     }
+  };
+  // the sub-tile's column-norm bound from the accumulated column sums (0 exactly when its B
+  // columns are all zero), shared through LDS
+  auto publish_nb = [&]() {
+    float bss = fmaxf(fmaxf(ssc[0], ssc[1]), fmaxf(ssc[2], ssc[3])), m = bmx;
     for (int off = 1; off < 64; off <<= 1) {
       bss = fmaxf(bss, __shfl_xor(bss, off));
-      bmx = fmaxf(bmx, __shfl_xor(bmx, off));
+      m = fmaxf(m, __shfl_xor(m, off));
     }
-    // 0 exactly when the sub-tile's B columns are all zero
-    if (lane == 0) nbs[wave] = norm_bound(bss, bmx, a.r);
-  }
-  __syncthreads();
-  float nbv[4];
+    if (lane == 0) nbs[wave] = norm_bound(bss, m, a.r);
+  };
+  // the lane's 8 ranks of its row (row l % 16, ranks 8 (l / 16) .. +7 of the chunk), through
+  // the wave's LDS rows
+  auto a_slice = [&](float (&xv)[8]) {
 #pragma unroll
-  for (int j = 0; j < 4; ++j) nbv[j] = nbs[j];
+    for (int h = 0; h < 2; ++h) *reinterpret_cast<u32x4*>(&arow[wave][8 * h + (lane >> 3)][4 * (lane & 7)]) = xc[h];
+    const f32x4 u = *reinterpret_cast<const f32x4*>(&arow[wave][lane & 15][8 * (lane >> 4)]);
+    const f32x4 w = *reinterpret_cast<const f32x4*>(&arow[wave][lane & 15][8 * (lane >> 4) + 4]);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      xv[e] = u[e];
+      xv[4 + e] = w[e];
+    }
+  };
+
+  float nbv[4];
+  f32x4 acc4[4][4];  // MULTI: the products of all rank chunks, per sub-tile
+  float ass = 0.f, amx = 0.f;
+  u32x4 ah, al;
+  if constexpr (!MULTI) {
+    stage_b(0);
+    publish_nb();
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < 4; ++j) nbv[j] = nbs[j];
+  } else {
+    // one round per block (nit = 1); every wave takes part in every barrier, also a wave whose
+    // rows lie past m (its loads read zeros and its stores are skipped)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int cb = 0; cb < 4; ++cb) acc4[j][cb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int ch = 0; ch < nks; ++ch) {
+      if (ch > 0) {
+        __syncthreads();  // every wave is done with the previous chunk's fragments
+        load_a_chunk(rb0, ch);
+      }
+      stage_b(ch);
+      __syncthreads();
+      float xv[8];
+      a_slice(xv);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        ass = __builtin_fmaf(xv[e], xv[e], ass);
+        amx = fmaxf(amx, fabsf(xv[e]));
+      }
+      split8(xv, ah, al);
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int cb = 0; cb < 4; ++cb) {
+          const u32x4 ph = bfrag[j][0][cb][lane], pl = bfrag[j][1][cb][lane];
+          acc4[j][cb] = mfma16(ph, ah, acc4[j][cb]);
+          acc4[j][cb] = mfma16(pl, ah, acc4[j][cb]);
+          acc4[j][cb] = mfma16(ph, al, acc4[j][cb]);
+        }
+    }
+    publish_nb();
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < 4; ++j) nbv[j] = nbs[j];
+  }
   const int64_t cl0_ = strip0 + 64 * g;  // the lane's first column
 
   int64_t rowblk = rb0;
   for (int it = 0; it < a.nit; ++it, rowblk += 4) {
-    if (rowblk * 16 >= a.m) break;  // wave-uniform
+    if (!MULTI && rowblk * 16 >= a.m) break;  // wave-uniform
     const int64_t row = rowblk * 16 + (lane & 15);
     // opaque per round, like the sub-tile index below: bounds and addresses derived
     // from the lane's columns are formed where they are used, not kept across rounds
     int64_t cl0 = cl0_;
     asm volatile("" : "+v"(cl0));
-    // through the wave's LDS rows: lane l takes row l % 16, ranks 8 (l / 16) .. +7
-#pragma unroll
-    for (int h = 0; h < 2; ++h) *reinterpret_cast<u32x4*>(&arow[wave][8 * h + (lane >> 3)][4 * (lane & 7)]) = xc[h];
-    float x[8];
-    {
-      const f32x4 u = *reinterpret_cast<const f32x4*>(&arow[wave][lane & 15][8 * (lane >> 4)]);
-      const f32x4 w = *reinterpret_cast<const f32x4*>(&arow[wave][lane & 15][8 * (lane >> 4) + 4]);
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        x[e] = u[e];
-        x[4 + e] = w[e];
-      }
-    }
     PhiRegs Pc[4];
+    if constexpr (!MULTI) {
+      float xv[8];
+      a_slice(xv);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) Pc[j] = P[j];
-    if (it + 1 < a.nit) load_round(rowblk + 4);
-    float ass = 0.f, amx = 0.f;
+      for (int j = 0; j < 4; ++j) Pc[j] = P[j];
+      if (it + 1 < a.nit) load_round(rowblk + 4);
+      ass = 0.f;
+      amx = 0.f;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      ass = __builtin_fmaf(x[e], x[e], ass);
-      amx = fmaxf(amx, fabsf(x[e]));
+      for (int e = 0; e < 8; ++e) {
+        ass = __builtin_fmaf(xv[e], xv[e], ass);
+        amx = fmaxf(amx, fabsf(xv[e]));
+      }
+      split8(xv, ah, al);
+    } else {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) Pc[j] = P[j];
     }
     // row norm: the 4 lanes l % 16 + 16 g hold the 4 rank slices of the row
-    ass += __shfl_xor(ass, 16);
-    ass += __shfl_xor(ass, 32);
-    amx = fmaxf(amx, __shfl_xor(amx, 16));
-    amx = fmaxf(amx, __shfl_xor(amx, 32));
-    const float na = norm_bound(ass, amx, a.r);
-    u32x4 ah, al;
-    split8(x, ah, al);
+    float rss = ass + __shfl_xor(ass, 16);
+    rss += __shfl_xor(rss, 32);
+    float rmx = fmaxf(amx, __shfl_xor(amx, 16));
+    rmx = fmaxf(rmx, __shfl_xor(rmx, 32));
+    const float na = norm_bound(rss, rmx, a.r);
     GridOut out[4];
 #pragma unroll 1
     for (int jl = 0; jl < 4; ++jl) {
@@ -888,16 +954,20 @@ __global__ __launch_bounds__(GR_THREADS) void k_grid_w(GridArgs a) {
       asm volatile("" : "+s"(j));
       PhiRegs Pj = Pc[0];
       float nb = nbv[0];
+      f32x4 acc[4];
+#pragma unroll
+      for (int cb = 0; cb < 4; ++cb) acc[cb] = MULTI ? acc4[0][cb] : f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int t = 1; t < 4; ++t)
         if (j == t) {
           nb = nbv[t];
           Pj = Pc[t];
+          if constexpr (MULTI) {
+#pragma unroll
+            for (int cb = 0; cb < 4; ++cb) acc[cb] = acc4[t][cb];
+          }
         }
       const int64_t c16 = cl0 + 16 * j;
-      f32x4 acc[4];
-#pragma unroll
-      for (int cb = 0; cb < 4; ++cb) acc[cb] = f32x4{0.f, 0.f, 0.f, 0.f};
       GridOut o;
       bool small = false;
       if constexpr (PACKED) {
@@ -909,15 +979,17 @@ __global__ __launch_bounds__(GR_THREADS) void k_grid_w(GridArgs a) {
       if (small) {
         grid_decide<PACKED, MASK, B4, Q8OUT>(a, Pj, acc, 0.f, false, row, c16, true, o);
       } else {
+        if constexpr (!MULTI) {
 #pragma unroll
-        for (int cb = 0; cb < 4; ++cb) {
-          const u32x4 ph = bfrag[j][0][cb][lane], pl = bfrag[j][1][cb][lane];
-          acc[cb] = mfma16(ph, ah, acc[cb]);
-          acc[cb] = mfma16(pl, ah, acc[cb]);
-          acc[cb] = mfma16(ph, al, acc[cb]);
+          for (int cb = 0; cb < 4; ++cb) {
+            const u32x4 ph = bfrag[j][0][cb][lane], pl = bfrag[j][1][cb][lane];
+            acc[cb] = mfma16(ph, ah, acc[cb]);
+            acc[cb] = mfma16(pl, ah, acc[cb]);
+            acc[cb] = mfma16(ph, al, acc[cb]);
+          }
         }
         // -1 where delta is exactly zero (a zero A row), so that no element is re-decided there
-        const float tau = amx == 0.f ? -1.f : a.tau_coef * na * nb;
+        const float tau = rmx == 0.f ? -1.f : a.tau_coef * na * nb;
         grid_decide<PACKED, MASK, B4, Q8OUT>(a, Pj, acc, tau, nb == 0.f, row, c16, false, o);
       }
 #pragma unroll
@@ -1059,35 +1131,52 @@ hipError_t launch_grid(const GridArgs& a0, hipStream_t st) {
   // 4-bit grids (the common W4 case) get an instantiation with the width fixed
   const int sel = (a.packed ? 8 : 0) | (a.r <= 32 ? 4 : 0) | (coal ? 2 : 0) | (a.mout ? 1 : 0);
   const bool b4 = a.bits == 4;
-  // wide tiles where they still give GRW_MIN_BLOCKS blocks: rounds of 64 rows per block,
-  // the most (up to 4) that keep that many
+  // wide tiles (r a multiple of 32, 16-byte aligned rows) where they still give GRW_MIN_BLOCKS
+  // blocks: rounds of 64 rows per block, the most (up to 4) that keep that many; r > 32
+  // accumulates its rank chunks in one round per block
   const int64_t nrb64 = (a.m + 63) / 64;
   const bool phi16 = ((a.ld_phi | int64_t(reinterpret_cast<uintptr_t>(a.phi0))) & 15) == 0;
-  if (coal && phi16 && nstrips * nrb64 >= GRW_MIN_BLOCKS) {
+  const bool wide_ok = a.r % 32 == 0 && a.k % 4 == 0 && (reinterpret_cast<uintptr_t>(a.A) & 15) == 0 &&
+                       (reinterpret_cast<uintptr_t>(a.B) & 15) == 0 && phi16;
+  if (wide_ok && nstrips * nrb64 >= GRW_MIN_BLOCKS) {
     GridArgs w = a;
-    w.nit = 4;
+    const bool multi = a.r > 32;
+    w.nit = multi ? 1 : 4;
     while (w.nit > 1 && nstrips * ((nrb64 + w.nit - 1) / w.nit) < GRW_MIN_BLOCKS) w.nit /= 2;
     const unsigned nbw = unsigned(nstrips * ((nrb64 + w.nit - 1) / w.nit));
-    const int wsel = (a.packed ? 4 : 0) | (a.mout ? 2 : 0) | (b4 ? 1 : 0);
+    const int wsel = (multi ? 8 : 0) | (a.packed ? 4 : 0) | (a.mout ? 2 : 0) | (b4 ? 1 : 0);
     if (a.q8out) {
       if (a.packed || a.bits <= 4) return hipErrorInvalidValue;
-      if (a.mout) k_grid_w<false, true, false, true><<<nbw, GR_THREADS, 0, st>>>(w);
-      else k_grid_w<false, false, false, true><<<nbw, GR_THREADS, 0, st>>>(w);
+      if (multi) {
+        if (a.mout) k_grid_w<false, true, false, true, true><<<nbw, GR_THREADS, 0, st>>>(w);
+        else k_grid_w<false, false, false, true, true><<<nbw, GR_THREADS, 0, st>>>(w);
+      } else {
+        if (a.mout) k_grid_w<false, true, false, true, false><<<nbw, GR_THREADS, 0, st>>>(w);
+        else k_grid_w<false, false, false, true, false><<<nbw, GR_THREADS, 0, st>>>(w);
+      }
       return hipGetLastError();
     }
     switch (wsel) {
-#define LRQAT_GRIDW_CASE(S, P, M, B)                                        \
+#define LRQAT_GRIDW_CASE(S, P, M, B, U)                                     \
   case S:                                                                   \
-    k_grid_w<P, M, B, false><<<nbw, GR_THREADS, 0, st>>>(w);                \
+    k_grid_w<P, M, B, false, U><<<nbw, GR_THREADS, 0, st>>>(w);             \
     break;
-      LRQAT_GRIDW_CASE(0, false, false, false)
-      LRQAT_GRIDW_CASE(1, false, false, true)
-      LRQAT_GRIDW_CASE(2, false, true, false)
-      LRQAT_GRIDW_CASE(3, false, true, true)
-      LRQAT_GRIDW_CASE(4, true, false, false)
-      LRQAT_GRIDW_CASE(5, true, false, true)
-      LRQAT_GRIDW_CASE(6, true, true, false)
-      LRQAT_GRIDW_CASE(7, true, true, true)
+      LRQAT_GRIDW_CASE(0, false, false, false, false)
+      LRQAT_GRIDW_CASE(1, false, false, true, false)
+      LRQAT_GRIDW_CASE(2, false, true, false, false)
+      LRQAT_GRIDW_CASE(3, false, true, true, false)
+      LRQAT_GRIDW_CASE(4, true, false, false, false)
+      LRQAT_GRIDW_CASE(5, true, false, true, false)
+      LRQAT_GRIDW_CASE(6, true, true, false, false)
+      LRQAT_GRIDW_CASE(7, true, true, true, false)
+      LRQAT_GRIDW_CASE(8, false, false, false, true)
+      LRQAT_GRIDW_CASE(9, false, false, true, true)
+      LRQAT_GRIDW_CASE(10, false, true, false, true)
+      LRQAT_GRIDW_CASE(11, false, true, true, true)
+      LRQAT_GRIDW_CASE(12, true, false, false, true)
+      LRQAT_GRIDW_CASE(13, true, false, true, true)
+      LRQAT_GRIDW_CASE(14, true, true, false, true)
+      LRQAT_GRIDW_CASE(15, true, true, true, true)
 #undef LRQAT_GRIDW_CASE
     }
     return hipGetLastError();
