@@ -860,16 +860,41 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
 
     // stage rank block rb of A (transposed) or B as bf16 [32][256] in `rt_tile`
     auto stage = [&](const float* __restrict__ src, bool is_a, int rb) {
-      const int rho_l = threadIdx.x >> 3, c0 = 32 * (threadIdx.x & 7);
-      const int rho = 32 * rb + rho_l;
       // unconditional buffer loads, all in flight at once: rows of A past M and ranks of B past r
       // lie outside the resource and read 0; ranks of A past r and columns of B past N are zeroed
       const auto rs = is_a ? rsrc(src + m0 * r, (p.M - m0) * int64_t(r) * 4) : rsrc(src + n0, (int64_t(r) * p.N - n0) * 4);
-      float xv[32];
+      if (is_a && (r & 3) == 0) {
+        // thread t takes row m0 + t: its 32 ranks as eight 16-byte loads, written transposed
+        const int c = threadIdx.x;
+        float xv[32];
 #pragma unroll
-      for (int i = 0; i < 32; ++i) {
-        const int c = c0 + i;
-        xv[i] = ldf(rs, is_a ? uint32_t((c * r + rho) * 4) : uint32_t((int64_t(rho) * p.N + c) * 4));
+        for (int q = 0; q < 8; ++q) {
+          const u32x4 v = ld128(rs, uint32_t((c * r + 32 * rb + 4 * q) * 4));
+#pragma unroll
+          for (int e = 0; e < 4; ++e) xv[4 * q + e] = __uint_as_float(v[e]);
+        }
+#pragma unroll
+        for (int rl = 0; rl < 32; ++rl)
+          rt_tile[g_off(rl, c)] = uint16_t(pack_bf16x2(32 * rb + rl < r ? xv[rl] : 0.f, 0.f) & 0xFFFFu);
+        return;
+      }
+      const int rho_l = threadIdx.x >> 3, c0 = 32 * (threadIdx.x & 7);
+      const int rho = 32 * rb + rho_l;
+      float xv[32];
+      if (!is_a && (p.N & 3) == 0) {
+        // B[rho][n0 + c0 .. +31]: eight 16-byte loads
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+          const u32x4 v = ld128(rs, uint32_t((int64_t(rho) * p.N + c0 + 4 * q) * 4));
+#pragma unroll
+          for (int e = 0; e < 4; ++e) xv[4 * q + e] = __uint_as_float(v[e]);
+        }
+      } else {
+#pragma unroll
+        for (int i = 0; i < 32; ++i) {
+          const int c = c0 + i;
+          xv[i] = ldf(rs, is_a ? uint32_t((c * r + rho) * 4) : uint32_t((int64_t(rho) * p.N + c) * 4));
+        }
       }
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
