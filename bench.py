@@ -51,6 +51,9 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU time of the oracle sample")
     ap.add_argument("--vendor-gemm", action="store_true",
                     help="only time the vendor library's plain bf16 GEMMs of the layer's three shapes and exit")
+    ap.add_argument("--rows", action="store_true",
+                    help="only time the rows after the hot path (scale gradient with a zero offset, inference "
+                         "on merged weights, the AdamW step, the L^p and LoftQ initialisations) and exit")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB (calibrates rocprofv3 byte counters) and exit")
     return ap.parse_args()
@@ -66,6 +69,109 @@ def copy_probe(mib):
         dst.copy_(src)
     torch.cuda.synchronize()
     print(json.dumps({"copy_probe_bytes_read": n * 4, "copy_probe_bytes_written": n * 4}), flush=True)
+
+
+def _time_us(fn, reps=20, warm=5):
+    import torch
+    for _ in range(warm):
+        fn()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        fn()
+    e1.record()
+    torch.cuda.synchronize()
+    return 1e3 * e0.elapsed_time(e1) / reps
+
+
+def rows_bench():
+    """The rows after the hot path, each on its paper-scale shape with seeded synthetic inputs:
+    the backward with the scale gradient and an asymmetric zero offset (vs without), inference on
+    the merged int4 weights (vs the training forward), the AdamW step over every adapter and scale
+    of a LLaMA-7B model, and the two setup-side initialisations."""
+    import torch
+    from paper_2406_06385_amd import inputs as I
+    from paper_2406_06385_amd import lrqat
+    lrqat.load_library()
+    dev = torch.device("cuda:0")
+    bf = lambda a: torch.from_numpy(a.view(np.int16).copy()).view(torch.bfloat16).to(dev)
+    out = {}
+    wl = I.WORKLOADS[2]
+    L0 = wl.layers[0]
+    T, m, k, r = wl.tokens, L0.m, L0.k, wl.rank
+    inp = I.make_layer_inputs(wl, 0)
+    W0 = torch.from_numpy(inp.W0).to(dev)
+    A, B = torch.from_numpy(inp.A).to(dev), torch.from_numpy(inp.B).to(dev)
+    X, dY = bf(inp.X), bf(inp.dY)
+    gemm_flop = 2.0 * T * m * k
+
+    # f1: backward with ds and z (asymmetric Q4.4), against the symmetric backward without ds
+    spec = lrqat.LayerSpec(m, k, r, wl.alpha, 4, "q8", 0, 0, "bf16")
+    s_sym, phi_sym = lrqat.lrqat_init_from_weights(spec, W0)
+    s_as, z_as, phi_as = lrqat.lrqat_init_from_weights(spec, W0, asymmetric=True)
+    dX = torch.empty_like(X)
+    dA, dB = torch.empty((m, r), device=dev), torch.empty((r, k), device=dev)
+    ds = torch.empty(s_as.shape, device=dev)
+    wb = lrqat.workspace(lrqat.lrqat_backward_workspace_size(spec, T), dev)
+    t_plain = _time_us(lambda: lrqat.lrqat_backward(spec, X, phi_sym, s_sym, A, B, dY, dX=dX, dA=dA, dB=dB, ws=wb))
+    t_ds = _time_us(lambda: lrqat.lrqat_backward(spec, X, phi_as, s_as, A, B, dY, dX=dX, dA=dA, dB=dB, ws=wb,
+                                                 z=z_as, ds=ds))
+    out["f1_backward_ds_z"] = {"layer": [m, k], "tokens": T, "us": t_ds, "us_without_ds_z": t_plain,
+                               "overhead": t_ds / t_plain - 1.0, "TFLOP/s": 2 * gemm_flop / (t_ds * 1e-6) / 1e12}
+
+    # f2: inference on the merged weights (packed INT4 Phi0 as for W_Z), against the training forward
+    spec4 = lrqat.LayerSpec(m, k, r, wl.alpha, 4, "int_packed2", 0, 0, "bf16")
+    s4, phi4 = lrqat.lrqat_init_from_weights(spec4, W0)
+    Wz = lrqat.lrqat_merge_to_int4(spec4, phi4, A, B)
+    Y = torch.empty((T, m), dtype=torch.bfloat16, device=dev)
+    wi = lrqat.workspace(lrqat.lrqat_infer_workspace_size(spec4, T), dev)
+    wf = lrqat.workspace(lrqat.lrqat_forward_workspace_size(spec4, T), dev)
+    t_inf = _time_us(lambda: lrqat.lrqat_infer_forward(spec4, X, Wz, s4, Y=Y, ws=wi))
+    t_fwd = _time_us(lambda: lrqat.lrqat_forward(spec4, X, phi4, s4, A, B, Y=Y, ws=wf))
+    out["f2_inference_merged_int4"] = {"layer": [m, k], "tokens": T, "us": t_inf, "TFLOP/s": gemm_flop / (t_inf * 1e-6) / 1e12,
+                                       "training_forward_us": t_fwd, "saved_by_merge_us": t_fwd - t_inf}
+    del Wz, wi, wf
+
+    # f3: AdamW over all adapters (A, B) and scales of a LLaMA-7B model at r = 32 (32 blocks of
+    # q, k, v, o 4096x4096 and gate, up 11008x4096, down 4096x11008), three parameter groups
+    shapes = [(4096, 4096)] * 4 + [(11008, 4096)] * 2 + [(4096, 11008)]
+    nA = 32 * sum(mm * r for mm, kk in shapes)
+    nB = 32 * sum(r * kk for mm, kk in shapes)
+    ns = 32 * sum(mm for mm, kk in shapes)
+    gen = torch.Generator(device=dev).manual_seed(7)
+    groups = []
+    for n, lr_max, wd in ((nA, 1e-3, 0.0), (nB, 1e-3, 0.0), (ns, 1e-5, 0.0)):
+        P = torch.randn(n, device=dev, generator=gen) * 0.01
+        groups.append(dict(param=P, grad=torch.randn(n, device=dev, generator=gen) * 1e-4,
+                           exp_avg=torch.zeros_like(P), exp_avg_sq=torch.zeros_like(P), lr_max=lr_max, weight_decay=wd))
+    step = [0]
+
+    def adam():
+        step[0] += 1
+        lrqat.lrqat_adamw_step(groups, step[0], 10000, 100)
+    t_adam = _time_us(adam)
+    nparam = nA + nB + ns
+    bytes_adam = nparam * (4 * 5 + 4 * 3)  # reads: g (norm pass and update), p, m, v; writes: p, m, v
+    out["f3_adamw_llama7b_adapters"] = {"params": nparam, "us": t_adam, "algorithmic_bytes": bytes_adam,
+                                        "GB/s": bytes_adam / (t_adam * 1e-6) / 1e9,
+                                        "frac_of_hbm_peak": bytes_adam / (t_adam * 1e-6) / 1e9 / PEAK_HBM_GBS}
+    del groups
+
+    # f4: L^p range search (p = 2.4, 100 candidates) on the q_proj layer; LoftQ (T = 1) on the MLP's
+    # gate projection, packed INT4, r = 32, 32 subspace iterations
+    specq = lrqat.LayerSpec(m, k, r, wl.alpha, 4, "q8", 0, 0, "bf16")
+    t_lp = _time_us(lambda: lrqat.lrqat_init_lp(specq, W0, 2.4, 100), reps=5, warm=1)
+    wl3 = I.WORKLOADS[3]
+    L3 = wl3.layers[0]
+    W3 = torch.from_numpy(I.gen_w0(L3.m, L3.k, 11, 12, 0.02, 0.0)).to(dev)
+    spec3 = lrqat.LayerSpec(L3.m, L3.k, 32, 32.0, 4, "int_packed2", 0, 0, "bf16")
+    s3, _ = lrqat.lrqat_init_from_weights(spec3, W3)
+    t_lq = _time_us(lambda: lrqat.lrqat_init_loftq(spec3, W3, s3, 32), reps=3, warm=1)
+    out["f4_init"] = {"lp_search": {"layer": [m, k], "p": 2.4, "candidates": 100, "us": t_lp,
+                                    "GB/s_of_W0": m * k * 4 / (t_lp * 1e-6) / 1e9},
+                      "loftq": {"layer": [L3.m, L3.k], "rank": 32, "iterations": 32, "us": t_lq}}
+    print(json.dumps({"rows": out}), flush=True)
 
 
 def vendor_gemm(wl):
@@ -179,6 +285,9 @@ def main():
     args = parse()
     if args.copy_probe:
         copy_probe(args.copy_probe)
+        return
+    if args.rows:
+        rows_bench()
         return
     if args.vendor_gemm:
         from paper_2406_06385_amd import inputs as I

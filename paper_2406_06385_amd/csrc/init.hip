@@ -137,43 +137,65 @@ template <bool TR>
 __global__ __launch_bounds__(256) void k_tsmm(const float* __restrict__ R, int64_t m, int64_t k,
                                               const float* __restrict__ V, int l, float* __restrict__ part,
                                               int64_t tchunk) {
-  __shared__ float rt[TS][TS + 1];  // rt[t][p]
-  __shared__ float vt[TS][64];      // vt[t][c]
+  // the 64 x 64 block of X: TR as rt[t][p] (pitch 68, 16-byte reads along p), else as rt[p][t]
+  // (pitch 65: the rows of R as they lie in memory, conflict-free column reads)
+  __shared__ __attribute__((aligned(16))) float rt[TS * 68];
+  __shared__ __attribute__((aligned(16))) float vt[TS][64];  // vt[t][c]
   const int64_t P = TR ? k : m, T = TR ? m : k;
   const int64_t p0 = int64_t(blockIdx.x) * TS;
   const int64_t t_begin = int64_t(blockIdx.y) * tchunk, t_end = min(T, t_begin + tchunk);
-  const int tp = threadIdx.x & 63, cg = threadIdx.x >> 6;  // p index, column group (columns cg, cg + 4, ...)
-  float acc[16];
+  // the thread's 4 x 4 register tile: rows p0 + 4 tp .. +3, columns 4 tc .. +3
+  const int tp = threadIdx.x & 15, tc = threadIdx.x >> 4;
+  float acc[4][4];
 #pragma unroll
-  for (int q = 0; q < 16; ++q) acc[q] = 0.f;
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = 0.f;
   for (int64_t t0 = t_begin; t0 < t_end; t0 += TS) {
-    // stage the 64 x 64 block of X and the 64 rows of V
+    // stage the block of R (reads along its contiguous index) and the 64 rows of V
     for (int e = threadIdx.x; e < TS * TS; e += 256) {
-      const int a = e >> 6, b = e & 63;  // a: the row of R inside the block, b: the column (coalesced)
-      int64_t ri, rj;
-      if (TR) { ri = t0 + a; rj = p0 + b; }  // X(p = b, t = a) = R[t][p]
-      else { ri = p0 + a; rj = t0 + b; }     // X(p = a, t = b) = R[p][t]
-      const float v = (ri < m && rj < k) ? R[ri * k + rj] : 0.f;
-      if (TR) rt[a][b] = v;
-      else rt[b][a] = v;
+      const int a = e >> 6, b = e & 63;
+      if (TR) {  // X(p, t) = R[t][p]: a = t, b = p
+        const int64_t ri = t0 + a, rj = p0 + b;
+        rt[a * 68 + b] = (ri < t_end && rj < k) ? R[ri * k + rj] : 0.f;
+      } else {   // X(p, t) = R[p][t]: a = p, b = t
+        const int64_t ri = p0 + a, rj = t0 + b;
+        rt[a * 65 + b] = (ri < m && rj < t_end) ? R[ri * k + rj] : 0.f;
+      }
     }
     for (int e = threadIdx.x; e < TS * 64; e += 256) {
       const int a = e >> 6, c = e & 63;
       vt[a][c] = (t0 + a < t_end && c < l) ? V[(t0 + a) * l + c] : 0.f;
     }
     __syncthreads();
+#pragma unroll 4
     for (int t = 0; t < TS; ++t) {
-      const float x = rt[t][tp];
+      float x[4];
+      if (TR) {
+        const f32x4 xv = *reinterpret_cast<const f32x4*>(&rt[t * 68 + 4 * tp]);
 #pragma unroll
-      for (int q = 0; q < 16; ++q) acc[q] = __builtin_fmaf(x, vt[t][cg + 4 * q], acc[q]);
+        for (int i = 0; i < 4; ++i) x[i] = xv[i];
+      } else {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) x[i] = rt[(4 * tp + i) * 65 + t];
+      }
+      const f32x4 y = *reinterpret_cast<const f32x4*>(&vt[t][4 * tc]);
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = __builtin_fmaf(x[i], y[j], acc[i][j]);
     }
     __syncthreads();
   }
-  if (p0 + tp < P) {
-    float* dst = part + (int64_t(blockIdx.y) * P + p0 + tp) * l;
 #pragma unroll
-    for (int q = 0; q < 16; ++q)
-      if (cg + 4 * q < l) dst[cg + 4 * q] = acc[q];
+  for (int i = 0; i < 4; ++i) {
+    const int64_t pp = p0 + 4 * tp + i;
+    if (pp < P) {
+      float* dst = part + (int64_t(blockIdx.y) * P + pp) * l;
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        if (4 * tc + j < l) dst[4 * tc + j] = acc[i][j];
+    }
   }
 }
 
@@ -219,60 +241,86 @@ __global__ __launch_bounds__(256) void k_gram_part(const float* __restrict__ Y, 
 }
 
 // One block: G = sum of the Gram partials; L = cholesky(G + eps tr(G) I); M = L^{-T} (float).
+// The factorisation is right-looking, one column per step with the trailing update spread over
+// the block; the inverse solves L X = I with one thread per column of X.
 __global__ __launch_bounds__(256) void k_chol_inv(const double* __restrict__ gpart, int64_t nparts, int l,
                                                   float* __restrict__ M) {
   __shared__ double G[64][65];
   __shared__ double Li[64][65];
+  __shared__ double shift_s;
   for (int e = threadIdx.x; e < l * l; e += 256) {
     const int a = e / l, b = e % l;
-    double s = 0.0;
-    for (int64_t q = 0; q < nparts; ++q) s += gpart[q * l * l + e];
-    G[a][b] = s;
+    double s0 = 0.0, s1 = 0.0;
+    int64_t q = 0;
+    for (; q + 2 <= nparts; q += 2) {
+      s0 += gpart[q * l * l + e];
+      s1 += gpart[(q + 1) * l * l + e];
+    }
+    if (q < nparts) s0 += gpart[q * l * l + e];
+    G[a][b] = s0 + s1;
   }
   __syncthreads();
   if (threadIdx.x == 0) {
     double tr = 0.0;
     for (int a = 0; a < l; ++a) tr += G[a][a];
-    const double shift = tr > 0.0 ? 1e-13 * tr : 1e-300;
-    for (int a = 0; a < l; ++a) G[a][a] += shift;
-    // in-place Cholesky, lower triangle
-    for (int j = 0; j < l; ++j) {
-      double d = G[j][j];
-      for (int q = 0; q < j; ++q) d -= G[j][q] * G[j][q];
-      d = d > 0.0 ? __builtin_sqrt(d) : 1e-150;
-      G[j][j] = d;
-      for (int i = j + 1; i < l; ++i) {
-        double v = G[i][j];
-        for (int q = 0; q < j; ++q) v -= G[i][q] * G[j][q];
-        G[i][j] = v / d;
-      }
+    shift_s = tr > 0.0 ? 1e-13 * tr : 1e-300;
+  }
+  __syncthreads();
+  if (threadIdx.x < l) G[threadIdx.x][threadIdx.x] += shift_s;
+  __syncthreads();
+  // lower triangle of G becomes L
+  for (int j = 0; j < l; ++j) {
+    if (threadIdx.x == 0) {
+      const double d = G[j][j];
+      G[j][j] = d > 0.0 ? __builtin_sqrt(d) : 1e-150;
     }
-    // Li = L^{-1} (lower triangular), column by column
-    for (int j = 0; j < l; ++j)
-      for (int i = 0; i < l; ++i) {
-        if (i < j) { Li[i][j] = 0.0; continue; }
-        double v = i == j ? 1.0 : 0.0;
-        for (int q = j; q < i; ++q) v -= G[i][q] * Li[q][j];
-        Li[i][j] = v / G[i][i];
+    __syncthreads();
+    const double dj = G[j][j];
+    for (int i = j + 1 + int(threadIdx.x); i < l; i += 256) G[i][j] /= dj;
+    __syncthreads();
+    // trailing update of the lower triangle: G[i][q] -= L[i][j] L[q][j], j < q <= i
+    const int nt = l - j - 1;
+    for (int e = threadIdx.x; e < nt * nt; e += 256) {
+      const int i = j + 1 + e / nt, q = j + 1 + e % nt;
+      if (q <= i) G[i][q] -= G[i][j] * G[q][j];
+    }
+    __syncthreads();
+  }
+  // Li = L^{-1}: column jc of Li by forward substitution, one thread per column
+  if (int(threadIdx.x) < l) {
+    const int jc = threadIdx.x;
+    for (int i = 0; i < l; ++i) {
+      if (i < jc) {
+        Li[i][jc] = 0.0;
+        continue;
       }
+      double v = i == jc ? 1.0 : 0.0;
+      for (int q = jc; q < i; ++q) v -= G[i][q] * Li[q][jc];
+      Li[i][jc] = v / G[i][i];
+    }
   }
   __syncthreads();
   // M = L^{-T}: M[a][b] = Li[b][a]
   for (int e = threadIdx.x; e < l * l; e += 256) M[e] = float(Li[e % l][e / l]);
 }
 
-// Y[row][:] <- Y[row][:] M (l x l), one thread per row.
+// Y[row][:] <- Y[row][:] M (l x l), one thread per row, the row in registers (l <= 64).
 __global__ __launch_bounds__(256) void k_apply(float* __restrict__ Y, int64_t P, int l, const float* __restrict__ M) {
   __shared__ float Ms[64][64];
-  for (int e = threadIdx.x; e < l * l; e += 256) Ms[e / l][e % l] = M[e];
+  for (int e = threadIdx.x; e < 64 * 64; e += 256) {
+    const int a = e >> 6, b = e & 63;
+    Ms[a][b] = (a < l && b < l) ? M[a * l + b] : 0.f;
+  }
   __syncthreads();
   const int64_t row = int64_t(blockIdx.x) * 256 + threadIdx.x;
   if (row >= P) return;
   float y[64];
-  for (int a = 0; a < l; ++a) y[a] = Y[row * l + a];
+#pragma unroll
+  for (int a = 0; a < 64; ++a) y[a] = a < l ? Y[row * l + a] : 0.f;
   for (int b = 0; b < l; ++b) {
     float s = 0.f;
-    for (int a = 0; a < l; ++a) s = __builtin_fmaf(y[a], Ms[a][b], s);
+#pragma unroll
+    for (int a = 0; a < 64; ++a) s = __builtin_fmaf(y[a], Ms[a][b], s);
     Y[row * l + b] = s;
   }
 }
