@@ -29,9 +29,27 @@ __global__ __launch_bounds__(OPT_THREADS) void k_sq_partials(OptimArgs a, double
   const int64_t c = blockIdx.x - first;
   const int64_t lo = c * OPT_CHUNK, hi = min(G.n, lo + OPT_CHUNK);
   double acc = 0.0;
-  for (int64_t j = lo + threadIdx.x; j < hi; j += OPT_THREADS) {
-    const double x = G.grad[j];
-    acc = __builtin_fma(x, x, acc);
+  if ((reinterpret_cast<uintptr_t>(G.grad) & 15) == 0) {
+    // 16-byte vectors (chunks start at multiples of 8192 elements), then the tail
+    const int64_t nv = (hi - lo) / 4;
+    double acc1 = 0.0;
+    for (int64_t i = threadIdx.x; i < nv; i += OPT_THREADS) {
+      const f32x4 v = *reinterpret_cast<const f32x4*>(G.grad + lo + 4 * i);
+      acc = __builtin_fma(double(v[0]), double(v[0]), acc);
+      acc1 = __builtin_fma(double(v[1]), double(v[1]), acc1);
+      acc = __builtin_fma(double(v[2]), double(v[2]), acc);
+      acc1 = __builtin_fma(double(v[3]), double(v[3]), acc1);
+    }
+    acc += acc1;
+    for (int64_t j = lo + 4 * nv + threadIdx.x; j < hi; j += OPT_THREADS) {
+      const double x = G.grad[j];
+      acc = __builtin_fma(x, x, acc);
+    }
+  } else {
+    for (int64_t j = lo + threadIdx.x; j < hi; j += OPT_THREADS) {
+      const double x = G.grad[j];
+      acc = __builtin_fma(x, x, acc);
+    }
   }
   for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
   __shared__ double red[OPT_THREADS / 64];
