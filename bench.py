@@ -294,8 +294,9 @@ def main():
         vendor_gemm(I.WORKLOADS[args.workload])
         return
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the multi-GPU path is not part "
-              f"of this build", file=sys.stderr)
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); runs on several GPUs are not "
+              f"implemented (the layer would shard along tokens with an all-reduce of dA, dB and ds)",
+              file=sys.stderr)
         sys.exit(2)
     import torch
 
