@@ -461,19 +461,17 @@ def main():
     W_int4 = [torch.empty((l["spec"].out_features, l["spec"].in_features // 2), dtype=torch.uint8, device=dev)
               for l in layers]
 
-    def merge_all():
-        # on the current stream (the capture stream inside a HIP graph)
-        for l, w in zip(layers, W_int4):
-            lrqat.lrqat_merge_to_int4(l["spec"], l["phi0"], l["A"], l["B"], out=w)
-
-    merge = None
-    if wl.bits <= 4:
+    def time_merge(Bs):
+        """Average time of merging every layer with adapters Bs (HIP-graph replays when the
+        step's graph check passed: eager launches of these short kernels measure the host)."""
+        def merge_all():
+            # on the current stream (the capture stream inside a HIP graph)
+            for l, w, b in zip(layers, W_int4, Bs):
+                lrqat.lrqat_merge_to_int4(l["spec"], l["phi0"], l["A"], b, out=w)
         for _ in range(3):
             merge_all()
         torch.cuda.synchronize()
-        merge_ref = [w.clone() for w in W_int4]
-        # timed as replays of one captured merge of every layer: eager launches of these
-        # short kernels measure the host's launch rate, not the GPU
+        ref_w = [w.clone() for w in W_int4]
         run, how = merge_all, "eager"
         if graph_ok:
             gm = torch.cuda.CUDAGraph()
@@ -483,7 +481,7 @@ def main():
                 w.fill_(0)
             gm.replay()
             torch.cuda.synchronize()
-            if all(torch.equal(w, r) for w, r in zip(W_int4, merge_ref)):
+            if all(torch.equal(w, r) for w, r in zip(W_int4, ref_w)):
                 run, how = gm.replay, "hip_graph"
         for _ in range(3):
             run()
@@ -493,10 +491,19 @@ def main():
             run()
         e1.record()
         torch.cuda.synchronize()
-        merge_us = 1e3 * e0.elapsed_time(e1) / 20
-        merge = {"us": merge_us, "layers": nl, "launch": how, "algorithmic_bytes": merge_bytes,
-                 "GB/s": merge_bytes / (merge_us * 1e-6) / 1e9,
-                 "frac_of_hbm_peak": merge_bytes / (merge_us * 1e-6) / 1e9 / PEAK_HBM_GBS}
+        us = 1e3 * e0.elapsed_time(e1) / 20
+        return {"us": us, "layers": nl, "launch": how, "algorithmic_bytes": merge_bytes,
+                "GB/s": merge_bytes / (us * 1e-6) / 1e9, "frac_of_hbm_peak": merge_bytes / (us * 1e-6) / 1e9 / PEAK_HBM_GBS}
+
+    merge = None
+    if wl.bits <= 4:
+        merge = time_merge([l["B"] for l in layers])
+        # the same merge with adapters as after training: B scaled so that delta has a standard
+        # deviation of about a quarter code (about 1% of the codes move), the exact paths engaged
+        b_scale = 5000.0
+        Bt = [l["B"] * b_scale for l in layers]
+        merge["trained_state"] = {"b_scale": b_scale, **time_merge(Bt)}
+        del Bt
     del W_int4
     src = torch.empty(256 << 18, dtype=torch.float32, device=dev)
     dst = torch.empty_like(src)

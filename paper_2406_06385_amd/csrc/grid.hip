@@ -279,10 +279,10 @@ __device__ __forceinline__ uint32_t pack_nibble_bytes(uint32_t q0, uint32_t q1) 
 //    itself.  Codes that would round off the grid send the wave on;
 //  * per element: with Phi0 = n + cf 2^-f (n = floor, cf the f fraction bits),
 //    u = n + 1/2 + w and w = (cf 2^-f - 1/2) + delta, one fused multiply-add of
-//    exact terms; for w in (-1, 1), w != 0, the nearest integer to u is
-//    n + [w > 0].  That is certain unless |w| lies within tau of 0 or is at
-//    least 1 - tau; a wave with such an element redoes its tile with exact
-//    margins and float64 deltas (rare).
+//    exact terms; for w strictly between the integers j - 1 and j the nearest
+//    integer to u is n + j = n + ceil(w).  That is certain unless w lies within
+//    the error bound of an integer; a wave with such an element redoes its tile
+//    with exact margins and float64 deltas (rare).
 // The lane's results for its 16 columns: q as 16 nibbles (w0, w1) or 16 bytes
 // (qb, Q8OUT), and the clip-mask bits.
 struct GridOut {
@@ -392,7 +392,7 @@ __device__ __forceinline__ void grid_decide(const GridArgs& a, const PhiRegs& P,
       ut[idx] = f ? n + int(cf > half || (cf == half && (n & 1))) : code;
     }
   } else {
-    const float tz = fmaxf(tau, 0.f), thr = 1.f - tz - 0x1p-22f;
+    const float tz = fmaxf(tau, 0.f);
     const float sf = __builtin_bit_cast(float, uint32_t(127 - f) << 23);  // 2^-f
     uint64_t flag = 0;
     // fraction bits of the four codes of each word, as unsigned bytes (Q8 only)
@@ -402,10 +402,12 @@ __device__ __forceinline__ void grid_decide(const GridArgs& a, const PhiRegs& P,
 #pragma unroll
     for (int idx = 0; idx < 16; ++idx) {
       const float x = PACKED ? -0.5f : __builtin_fmaf(float((fw[idx >> 2] >> (8 * (idx & 3))) & 0xffu), sf, -0.5f);
+      // u = n + 1/2 + w: for w in (j - 1, j), j an integer, the nearest integer to u is n + j =
+      // n + ceil(w); certain unless w lies within the bound of an integer (the bound adds the
+      // rounding of this fused multiply-add, below 2^-24 |w|, doubled)
       const float w = __builtin_fmaf(acc[idx >> 2][idx & 3], a.c, x);
-      flag |= __builtin_amdgcn_ballot_w64(fabsf(w) <= tz);
-      flag |= __builtin_amdgcn_ballot_w64(fabsf(w) >= thr);
-      ut[idx] = n_of(idx) + int(w > 0.f);
+      flag |= __builtin_amdgcn_ballot_w64(fabsf(w - __builtin_rintf(w)) <= __builtin_fmaf(0x1p-23f, fabsf(w), tz));
+      ut[idx] = n_of(idx) + int(__builtin_ceilf(w));
     }
     if (flag) {
       // exact margins and float64 re-decision for the lanes' elements within the bound
