@@ -4,11 +4,14 @@
 
 A step is lrqat_forward followed by lrqat_backward (dX, dA, dB) for every linear
 of the workload, each on its own batch of seeded synthetic inputs already
-resident in device memory.  The step is captured once in a HIP graph and
-replayed (each replay checked bit for bit against an eager step); the eager
-rate is reported beside it, and the per-kernel times come from eager steps.  The default workload is the LLaMA-7B q_proj-shaped
-layer 4096 -> 4096 with 8 x 1024 tokens, rank 32, alpha 32, W4 per-channel and
-Phi0 in fixed point Q4.4.  Prints one JSON line.
+resident in device memory.  The value is the rate of eager launches on one
+stream; the same step is also captured once in a HIP graph and replayed (each
+replay checked bit for bit against an eager step), its rate reported beside
+it, and the per-kernel times come from eager steps.
+The default 500 warm-up steps bring the clocks to their steady state (a short
+warm-up times a clock that is still rising).  The default workload is the
+LLaMA-7B q_proj-shaped layer 4096 -> 4096 with 8 x 1024 tokens, rank 32,
+alpha 32, W4 per-channel and Phi0 in fixed point Q4.4.  Prints one JSON line.
 
 value = algorithmic flops per step (sum over the layers of 6 T m k + 8 m k r)
 / step time, in TFLOP/s.
@@ -42,8 +45,8 @@ PEAK_HBM_GBS = 8000.0
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=100)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=500)
     ap.add_argument("--workload", type=int, default=2)
     ap.add_argument("--rank", type=int, default=0, help="override the workload's rank r (and alpha = r)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -368,6 +371,17 @@ def main():
     print(f"[bench] warmup done ({args.warmup} steps)", file=sys.stderr, flush=True)
 
     def time_steps(run):
+        """(ms per step over K steps bracketed by one pair of events, per-step ms from a second
+        pass of K steps with an event after each; events between graph launches can delay
+        them, so the mean comes from the pass without)."""
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(args.steps):
+            run()
+        e1.record()
+        torch.cuda.synchronize()
+        ms_mean = e0.elapsed_time(e1) / args.steps
         evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
         torch.cuda.synchronize()
         evs[0].record()
@@ -375,8 +389,7 @@ def main():
             run()
             evs[i + 1].record()
         torch.cuda.synchronize()
-        return evs[0].elapsed_time(evs[-1]) / args.steps, np.array([evs[i].elapsed_time(evs[i + 1])
-                                                                    for i in range(args.steps)])
+        return ms_mean, np.array([evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps)])
 
     ms_eager, per_step_eager = time_steps(step)
     # device memory of the training steps themselves (before the graph-check copies below)
@@ -409,11 +422,13 @@ def main():
             graph_note = "replays bit-identical to the eager step" if graph_ok else "replay differs: eager timing used"
         except Exception as e:  # pragma: no cover - capture unsupported
             graph_ok, graph_note = False, f"capture failed: {type(e).__name__}: {e}"
+    # the value is the eager rate (the library's ordinary use); the graph replays run the same
+    # kernels and are reported beside it
+    ms, per_step = ms_eager, per_step_eager
+    ms_graph, per_step_graph = None, None
     if graph_ok:
-        ms, per_step = time_steps(g.replay)
-        print(f"[bench] timed {args.steps} graph replays: {ms:.4f} ms/step", file=sys.stderr, flush=True)
-    else:
-        ms, per_step = ms_eager, per_step_eager
+        ms_graph, per_step_graph = time_steps(g.replay)
+        print(f"[bench] timed {args.steps} graph replays: {ms_graph:.4f} ms/step", file=sys.stderr, flush=True)
     peak_mem = torch.cuda.max_memory_allocated(dev)
     flops = wl.flops_fwd_bwd()
     value = flops / (ms * 1e-3) / 1e12
@@ -472,26 +487,29 @@ def main():
             merge_all()
         torch.cuda.synchronize()
         ref_w = [w.clone() for w in W_int4]
-        run, how = merge_all, "eager"
+        # ten merges per graph, so that the replays' own launch gaps are amortised
+        run, how, per_run = merge_all, "eager", 1
         if graph_ok:
             gm = torch.cuda.CUDAGraph()
             with torch.cuda.graph(gm):
-                merge_all()
+                for _ in range(10):
+                    merge_all()
             for w in W_int4:
                 w.fill_(0)
             gm.replay()
             torch.cuda.synchronize()
             if all(torch.equal(w, r) for w, r in zip(W_int4, ref_w)):
-                run, how = gm.replay, "hip_graph"
-        for _ in range(3):
+                run, how, per_run = gm.replay, "hip_graph", 10
+        for _ in range(2):
             run()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        nrun = 40 // per_run
         e0.record()
-        for _ in range(20):
+        for _ in range(nrun):
             run()
         e1.record()
         torch.cuda.synchronize()
-        us = 1e3 * e0.elapsed_time(e1) / 20
+        us = 1e3 * e0.elapsed_time(e1) / (nrun * per_run)
         return {"us": us, "layers": nl, "launch": how, "algorithmic_bytes": merge_bytes,
                 "GB/s": merge_bytes / (us * 1e-6) / 1e9, "frac_of_hbm_peak": merge_bytes / (us * 1e-6) / 1e9 / PEAK_HBM_GBS}
 
@@ -543,8 +561,10 @@ def main():
                    "alpha": wl.alpha, "bits": wl.bits, "phi_format": wl.phi_format, "group_size": wl.group_size,
                    "act_bits": wl.act_bits, "parallelism": "none"},
         "step_ms_p10_p50_p90": [float(np.percentile(per_step, q)) for q in (10, 50, 90)],
-        "launch": "hip_graph" if graph_ok else "eager", "hip_graph": graph_note,
-        "ms_per_step_eager": ms_eager,
+        "launch": "eager",
+        "hip_graph": {"note": graph_note, "ms_per_step": ms_graph,
+                      "step_ms_p10_p50_p90": [float(np.percentile(per_step_graph, q)) for q in (10, 50, 90)]
+                      if per_step_graph is not None else None},
         "pct_of_bf16_peak": 100.0 * value / PEAK_BF16_TFLOPS,
         "tokens_per_s": T / (ms * 1e-3),
         "peak_device_mem_bytes": int(peak_mem_steps),
