@@ -15,7 +15,8 @@
 // Block tile 256 x 256 x 64, four waves in a 2 x 2 arrangement, each wave a
 // 128 x 128 sub-tile of 4 x 4 MFMA 32x32x16 blocks.  Two LDS stages of
 // (256 + 256) x 64 bfloat16 (128 KiB); the next K-tile is fetched into
-// registers while the current one feeds the MFMAs.
+// registers while the current one feeds the MFMAs.  The forward and dX output
+// tiles leave through LDS as whole row segments.
 #pragma once
 
 #include "kernels.h"
@@ -440,8 +441,8 @@ struct Loader<kDw, ACT, GRP, VEC, OPT> {
   }
 };
 
-// Offset of element (i, j) in a [rows][256] bfloat16 staging tile of the dW
-// epilogue (G, and the B block): the 32 16-byte chunks of a 512-byte row are
+// Offset of element (i, j) in a [rows][256] bfloat16 staging tile of an
+// epilogue (the output tile; dW's G and its A/B blocks): the 32 16-byte chunks of a 512-byte row are
 // permuted by i mod 32, so 32 consecutive rows read at one column hit 32
 // different chunk slots.
 __device__ __forceinline__ int g_off(int i, int j) { return i * 256 + ((((j >> 3) ^ (i & 31))) << 3) + (j & 7); }
@@ -723,6 +724,42 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
 #pragma unroll
         for (int e = 0; e < 4; ++e) cs[j][g][e] = (V == kFwd && !GRP && c + e < p.N) ? p.s[c + e] : 1.f;
       }
+    if ((p.ldo & 7) == 0 && (p.N & 7) == 0 && (reinterpret_cast<uintptr_t>(out) & 15) == 0) {
+      // The tile goes through LDS (bf16 [256][256], 16-byte chunks permuted by
+      // row as in g_off) and back to memory as whole 512-byte row segments: a
+      // store instruction then covers two rows instead of 16 bytes of 32 rows,
+      // which shortens the burst of output writes that ends the kernel.
+      __syncthreads();  // every wave has read its last fragments
+      uint16_t* Cs = lds;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int lr = wm + 32 * i + (lane & 31);
+        const float rs = (V == kFwd && ACT && m0 + lr < p.M) ? p.sx[m0 + lr] : 1.f;
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+          for (int g = 0; g < 4; ++g) {
+            float val[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) val[e] = acc[i][j][4 * g + e] * cs[j][g][e] * rs;
+            *reinterpret_cast<u32x2*>(Cs + g_off(lr, wn + 32 * j + 8 * g + 4 * (lane >> 5))) =
+                u32x2{pack_bf16x2(val[0], val[1]), pack_bf16x2(val[2], val[3])};
+          }
+      }
+      __syncthreads();
+      // thread t writes 16-byte chunk t % 32 of rows 8 ps + t / 32
+      const int ch = threadIdx.x & 31;
+      const int64_t col = n0 + 8 * ch;
+      if (col < p.N) {
+#pragma unroll 8
+        for (int ps = 0; ps < 32; ++ps) {
+          const int lr = 8 * ps + (threadIdx.x >> 5);
+          const u32x4 v = *reinterpret_cast<const u32x4*>(Cs + g_off(lr, 8 * ch));
+          if (m0 + lr < p.M) *reinterpret_cast<u32x4*>(out + (m0 + lr) * p.ldo + col) = v;
+        }
+      }
+      return;
+    }
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int64_t row = row_l + 32 * i;

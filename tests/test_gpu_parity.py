@@ -296,6 +296,7 @@ SMALL = [
     (256, 256, 64, 256, 256.0, 4, "q8", 0, 0, "bf16"),      # r = 256
     (96, 64, 1, 8, 8.0, 2, "q8", 32, 0, "bf16"),            # T = 1, Q2.6, g32
     (128, 256, 40, 8, 8.0, 3, "q8", 64, 8, "bf16"),
+    (203, 140, 50, 8, 8.0, 4, "int_packed2", 0, 0, "bf16"),  # m, k not multiples of 8: per-lane output stores
 ]
 
 
