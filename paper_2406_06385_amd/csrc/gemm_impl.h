@@ -488,10 +488,10 @@ enum : int { kPipeSpread = 0, kPipeOneSet = 1, kPipeTile = 2 };
 template <int V>
 struct Sched {
   static constexpr int kPipe = kPipeSpread;
-  static constexpr int kLoadStep = V == kFwd ? 1 : V == kDx ? 0 : 2;
-  static constexpr int kValu = V == kFwd ? 4 : V == kDx ? 2 : 5;
+  static constexpr int kLoadStep = 1;
+  static constexpr int kValu = V == kFwd ? 4 : 3;
   static constexpr int kWritesPerPair = 1;
-  static constexpr int kVmemPerMfma = 2;
+  static constexpr int kVmemPerMfma = 1;
 };
 
 template <class S, bool VMEM, bool WRITES>
