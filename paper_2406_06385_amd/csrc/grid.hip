@@ -781,6 +781,7 @@ __global__ __launch_bounds__(GR_THREADS) void k_grid_w(GridArgs a) {
   __shared__ __attribute__((aligned(16))) u32x4 bfrag[4][2][4][64];
   __shared__ __attribute__((aligned(16))) float arow[4][16][36];  // the wave's A rows (144-byte pitch)
   __shared__ float nbs[4];                                         // column-norm bound per sub-tile
+  __shared__ float cnb[4], cna[4];                                 // block-wide copy test: B and A norm bounds per wave
 
   // round 0's codes and A rows first: they do not depend on the B fragments
   PhiRegs P[4];
@@ -804,22 +805,20 @@ __global__ __launch_bounds__(GR_THREADS) void k_grid_w(GridArgs a) {
   // 16 q + c) in the wave's fragment region, then read back in operand order.  ssc[cb]
   // accumulates the squared norm of the lane's column of block cb, bmx the largest |B|.
   float ssc[4] = {0.f, 0.f, 0.f, 0.f}, bmx = 0.f;
-  auto stage_b = [&](int ch) {
-    float* raw = reinterpret_cast<float*>(&bfrag[wave][0][0][0]);
+  auto load_b = [&](int ch, u32x4 (&v)[8]) {
     const auto rb = grid_rsrc(a.B + strip0, int64_t(a.r) * a.k * 4 - strip0 * 4);
-    const int cl = 4 * (lane & 15);                                             // raw position
     const int64_t gc = 64 * ((lane & 15) >> 2) + 16 * wave + 4 * (lane & 3);  // strip column
-    u32x4 v[8];
 #pragma unroll
     for (int t = 0; t < 8; ++t)
       v[t] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
                                            rb, int(uint32_t(((32 * ch + 4 * t + (lane >> 4)) * a.k + gc) * 4)), 0, 0));
 #pragma unroll
-    for (int t = 0; t < 8; ++t) {
+    for (int t = 0; t < 8; ++t)
 #pragma unroll
       for (int j = 0; j < 4; ++j) v[t][j] = strip0 + gc + j < a.k ? v[t][j] : 0u;
-      *reinterpret_cast<u32x4*>(raw + (4 * t + (lane >> 4)) * 64 + cl) = v[t];
-    }
+  };
+  auto stage_b_tail = [&]() {
+    const float* raw = reinterpret_cast<const float*>(&bfrag[wave][0][0][0]);
     float y[4][8];
     float ss[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -840,6 +839,31 @@ __global__ __launch_bounds__(GR_THREADS) void k_grid_w(GridArgs a) {
       ss[cb] += __shfl_xor(ss[cb], 32);
       ssc[cb] += ss[cb];
     }
+  };
+  auto stage_b_from = [&](const u32x4 (&v)[8]) {
+    float* raw = reinterpret_cast<float*>(&bfrag[wave][0][0][0]);
+    const int cl = 4 * (lane & 15);  // raw position
+#pragma unroll
+    for (int t = 0; t < 8; ++t) *reinterpret_cast<u32x4*>(raw + (4 * t + (lane >> 4)) * 64 + cl) = v[t];
+    stage_b_tail();
+  };
+  auto stage_b = [&](int ch) {
+    float* raw = reinterpret_cast<float*>(&bfrag[wave][0][0][0]);
+    const auto rb = grid_rsrc(a.B + strip0, int64_t(a.r) * a.k * 4 - strip0 * 4);
+    const int cl = 4 * (lane & 15);                                             // raw position
+    const int64_t gc = 64 * ((lane & 15) >> 2) + 16 * wave + 4 * (lane & 3);  // strip column
+    u32x4 v[8];
+#pragma unroll
+    for (int t = 0; t < 8; ++t)
+      v[t] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                                           rb, int(uint32_t(((32 * ch + 4 * t + (lane >> 4)) * a.k + gc) * 4)), 0, 0));
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) v[t][j] = strip0 + gc + j < a.k ? v[t][j] : 0u;
+      *reinterpret_cast<u32x4*>(raw + (4 * t + (lane >> 4)) * 64 + cl) = v[t];
+    }
+    stage_b_tail();
   };
   // the sub-tile's column-norm bound from the accumulated column sums (0 exactly when its B
   // columns are all zero), shared through LDS
@@ -865,12 +889,159 @@ __global__ __launch_bounds__(GR_THREADS) void k_grid_w(GridArgs a) {
     }
   };
 
+  // q [row][cl0 .. cl0 + 63] (and the mask words) of one round, as the round loop below stores
+  // them (which keeps its own copy of these stores: through this lambda it needs more registers)
+  auto store_round = [&](int64_t row, int64_t cl0, const GridOut (&out)[4]) {
+    const bool whole = row < a.m && cl0 + 64 <= a.kq;
+    if constexpr (Q8OUT) {
+      uint8_t* dst = a.qout + row * a.ldq + cl0;
+      if (whole && (reinterpret_cast<uintptr_t>(dst) & 15) == 0) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          *reinterpret_cast<u32x4*>(dst + 16 * j) = u32x4{out[j].qb[0], out[j].qb[1], out[j].qb[2], out[j].qb[3]};
+      } else {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) grid_store<false, true>(a, out[j], row, cl0 + 16 * j);
+      }
+    } else {
+      uint8_t* dst = a.qout + row * a.ldq + (cl0 >> 1);
+      if (whole && (reinterpret_cast<uintptr_t>(dst) & 15) == 0) {
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+          *reinterpret_cast<u32x4*>(dst + 16 * h) =
+              u32x4{out[2 * h].w0, out[2 * h].w1, out[2 * h + 1].w0, out[2 * h + 1].w1};
+      } else {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) grid_store<false, false>(a, out[j], row, cl0 + 16 * j);
+      }
+    }
+    if constexpr (MASK) {
+      uint16_t* md = a.mout + row * a.ldm + (cl0 >> 4);
+      if (whole && (reinterpret_cast<uintptr_t>(md) & 7) == 0) {
+        *reinterpret_cast<u32x2*>(md) =
+            u32x2{(out[0].mb & 0xFFFFu) | (out[1].mb << 16), (out[2].mb & 0xFFFFu) | (out[3].mb << 16)};
+      } else if (row < a.m) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          if (cl0 + 16 * j < a.kq) md[j] = uint16_t(out[j].mb);
+      }
+    }
+  };
+
   float nbv[4];
   f32x4 acc4[4][4];  // MULTI: the products of all rank chunks, per sub-tile
   float ass = 0.f, amx = 0.f;
   u32x4 ah, al;
   if constexpr (!MULTI) {
-    stage_b(0);
+    u32x4 bv[8];
+    if constexpr (PACKED) load_b(0, bv);
+    else stage_b(0);
+    if constexpr (PACKED) {
+      // Integer Phi0 on a 4-bit grid: when |c| max_i ||A_i|| max_j ||B_j|| over all rows of the
+      // block's rounds and all columns of its strip is below 1/2, every sub-tile has q = Phi0 and
+      // nothing clips (the per-sub-tile test below would pass everywhere), so the block copies
+      // Phi0 without staging B fragments.  The test uses maxima of the same norm bounds.
+      if (B4 || a.bits == 4) {
+        // column sums of squares of the wave's sub-tile, straight from the loaded values: lanes
+        // l, l ^ 16, l ^ 32, l ^ 48 hold the 32 ranks of the same 4 columns
+        float cs[4] = {0.f, 0.f, 0.f, 0.f}, m = 0.f;
+#pragma unroll
+        for (int t = 0; t < 8; ++t)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const float x = __uint_as_float(bv[t][j]);
+            cs[j] = __builtin_fmaf(x, x, cs[j]);
+            m = fmaxf(m, fabsf(x));
+          }
+        float bss = 0.f;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          cs[j] += __shfl_xor(cs[j], 16);
+          cs[j] += __shfl_xor(cs[j], 32);
+          bss = fmaxf(bss, cs[j]);
+        }
+        // largest row sum of squares of 16 A rows held as the round's chunks (lanes 8 e .. 8 e + 7
+        // hold the eight 16-byte chunks of rows e and 8 + e)
+        float ras = 0.f, ram = 0.f;
+        auto rows_max = [&](const u32x4 (&v)[2]) {
+#pragma unroll
+          for (int h = 0; h < 2; ++h) {
+            float ss = 0.f, mx = 0.f;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const float x = __uint_as_float(v[h][e]);
+              ss = __builtin_fmaf(x, x, ss);
+              mx = fmaxf(mx, fabsf(x));
+            }
+#pragma unroll
+            for (int off = 1; off < 8; off <<= 1) {
+              ss += __shfl_xor(ss, off);
+              mx = fmaxf(mx, __shfl_xor(mx, off));
+            }
+            ras = fmaxf(ras, ss);
+            ram = fmaxf(ram, mx);
+          }
+        };
+        auto wave_max = [&](float& x) {
+          for (int off = 1; off < 64; off <<= 1) x = fmaxf(x, __shfl_xor(x, off));
+        };
+        // first with round 0's rows (their A chunk is loaded): a block whose B columns and first
+        // rows already exceed the bound goes on without loading the other rounds' rows
+        rows_max(xc);
+        wave_max(bss);
+        wave_max(m);
+        wave_max(ras);
+        wave_max(ram);
+        if (lane == 0) {
+          cnb[wave] = norm_bound(bss, m, a.r);
+          cna[wave] = norm_bound(ras, ram, a.r);
+        }
+        __syncthreads();
+        const float nbm = fmaxf(fmaxf(cnb[0], cnb[1]), fmaxf(cnb[2], cnb[3]));
+        const float lim = 0.5f - 0x1p-20f;
+        if (fabsf(a.c) * fmaxf(fmaxf(cna[0], cna[1]), fmaxf(cna[2], cna[3])) * nbm * 1.02f < lim) {  // block-uniform
+          // the other rounds' rows, and every round's codes, in flight at once (rows past m read 0)
+          PhiRegs Pr[4][4];
+#pragma unroll
+          for (int j = 0; j < 4; ++j) Pr[0][j] = P[j];
+          u32x4 av[4][2];
+#pragma unroll
+          for (int it = 1; it < 4; ++it) {
+            const int64_t rblk = rb0 + 4 * it;
+            const auto r = grid_rsrc(a.A + rblk * 16 * a.r, it < a.nit ? (a.m - rblk * 16) * int64_t(a.r) * 4 : 0);
+#pragma unroll
+            for (int h = 0; h < 2; ++h)
+              av[it][h] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                                                        r, int(uint32_t((8 * h + (lane >> 3)) * a.r * 4 + 16 * (lane & 7))), 0, 0));
+            if (it < a.nit) load_phi_w<PACKED>(Pr[it], a, rblk, strip0);
+          }
+#pragma unroll
+          for (int it = 1; it < 4; ++it) rows_max(av[it]);
+          wave_max(ras);
+          wave_max(ram);
+          __syncthreads();  // every wave has read the first round's values
+          if (lane == 0) cna[wave] = norm_bound(ras, ram, a.r);
+          __syncthreads();
+          const float nam = fmaxf(fmaxf(cna[0], cna[1]), fmaxf(cna[2], cna[3]));
+          if (fabsf(a.c) * nam * nbm * 1.02f < lim) {  // block-uniform
+            const f32x4 zero[4] = {};
+#pragma unroll
+            for (int it = 0; it < 4; ++it) {
+              const int64_t rowblk = rb0 + 4 * it;
+              if (it >= a.nit || rowblk * 16 >= a.m) break;  // wave-uniform
+              const int64_t row = rowblk * 16 + (lane & 15);
+              GridOut out[4];
+#pragma unroll
+              for (int j = 0; j < 4; ++j)
+                grid_decide<PACKED, MASK, B4, Q8OUT>(a, Pr[it][j], zero, 0.f, false, row, strip0 + 64 * g + 16 * j, true, out[j]);
+              store_round(row, strip0 + 64 * g, out);
+            }
+            return;
+          }
+        }
+      }
+    }
+    if constexpr (PACKED) stage_b_from(bv);
     publish_nb();
     __syncthreads();
 #pragma unroll
