@@ -121,3 +121,29 @@ def test_wide_six_bit_grid_int8_q(lr, r):
     c = Case(lr, M, K, T, r, float(r), 6, "q8", 0, 0, "bf16", seed=71, b_std=0.05, a_scale=8.0)
     check_setup(c)
     check_full(lr, c)
+
+
+@pytest.mark.parametrize("variant", ["copy", "late_rows"])
+def test_wide_packed_copy_regime_rounds(lr, variant):
+    """Packed INT4 Phi0 with r = 32 at m = 7750, k = 4224: four 16-row rounds per wave, rows past
+    m in the last blocks' later rounds, a ragged last strip.  'copy': the adapters' product is
+    far below 1/2 everywhere, so every block copies Phi0 (the block-wide Cauchy-Schwarz test);
+    'late_rows': rows 64..255 of every 256 (the second to fourth rounds of each block) are
+    scaled up, so a block passes the test on its first round's rows and fails it on the
+    others, and goes on to the per-sub-tile decisions."""
+    m, k = 7750, 4224
+    _log(f"[wide packed copy regime {variant}]")
+    c = Case(lr, m, k, 64, 32, 32.0, 4, "int_packed2", 0, 0, "bf16", seed=83)
+    if variant == "late_rows":
+        rows = (np.arange(m) % 256) >= 64
+        c.A[rows] *= np.float32(3000.0)
+        c.d_A = torch.from_numpy(c.A).cuda()
+    check_setup(c)
+    q_ref, near = check_merge(lr, c, allow_near=variant == "late_rows")
+    phi = O.decode_phi0(c.phi0_ref, 4, "int_packed2")
+    moved = int((q_ref != phi).sum())
+    if variant == "copy":
+        assert moved == 0
+    else:
+        assert moved > 1000, "the scaled rows should move codes"
+    check_full(lr, c)
