@@ -847,6 +847,8 @@ __global__ __launch_bounds__(GR_THREADS) void k_grid_w(GridArgs a) {
     for (int t = 0; t < 8; ++t) *reinterpret_cast<u32x4*>(raw + (4 * t + (lane >> 4)) * 64 + cl) = v[t];
     stage_b_tail();
   };
+  // load_b + stage_b_from in one, with each raw write next to its load (the byte-parallel and
+  // multi-chunk paths keep this form: split, they need more registers)
   auto stage_b = [&](int ch) {
     float* raw = reinterpret_cast<float*>(&bfrag[wave][0][0][0]);
     const auto rb = grid_rsrc(a.B + strip0, int64_t(a.r) * a.k * 4 - strip0 * 4);
