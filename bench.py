@@ -8,8 +8,9 @@ resident in device memory.  The value is the rate of eager launches on one
 stream; the same step is also captured once in a HIP graph and replayed (each
 replay checked bit for bit against an eager step), its rate reported beside
 it, and the per-kernel times come from eager steps.
-The default 500 warm-up steps bring the clocks to their steady state (a short
-warm-up times a clock that is still rising).  The default workload is the
+Before the W warm-up steps the step runs, untimed, for --settle-ms of wall time
+(reported as clock_settle): the GPU's clocks rise over the first few hundred
+steps, and a short warm-up would time a clock that is still rising.  The default workload is the
 LLaMA-7B q_proj-shaped layer 4096 -> 4096 with 8 x 1024 tokens, rank 32,
 alpha 32, W4 per-channel and Phi0 in fixed point Q4.4.  Prints one JSON line.
 
@@ -47,6 +48,8 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=500)
+    ap.add_argument("--settle-ms", type=float, default=400.0,
+                    help="untimed repetitions of the step for this long before the warm-up steps (0: none)")
     ap.add_argument("--workload", type=int, default=2)
     ap.add_argument("--rank", type=int, default=0, help="override the workload's rank r (and alpha = r)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -363,7 +366,19 @@ def main():
         return all(torch.equal(x.view(torch.int16) if x.dtype == torch.bfloat16 else x,
                                y.view(torch.int16) if y.dtype == torch.bfloat16 else y) for x, y in zip(a, b))
 
+    # clock settle: the step repeated, untimed, for a fixed wall time before the warm-up steps, so
+    # that the timed steps do not run while the GPU's clocks are still rising from idle
     torch.cuda.synchronize()
+    settle_steps, t_settle = 0, time.perf_counter()
+    while (time.perf_counter() - t_settle) * 1e3 < args.settle_ms:
+        for _ in range(10):
+            step()
+        settle_steps += 10
+        torch.cuda.synchronize()
+    settle = {"steps": settle_steps, "ms": (time.perf_counter() - t_settle) * 1e3,
+              "note": "untimed repetitions of the step before the warm-up steps (clocks rise over the first "
+                      "few hundred steps)"}
+    print(f"[bench] clock settle: {settle_steps} steps in {settle['ms']:.0f} ms", file=sys.stderr, flush=True)
     torch.cuda.reset_peak_memory_stats(dev)
     for _ in range(args.warmup):
         step()
@@ -555,6 +570,7 @@ def main():
     out = {
         "metric": METRIC, "value": value, "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+        "clock_settle": settle,
         "vs_baseline": None, "dtype": "bf16" if wl.act_dtype == "bf16" else "fp32", "data": "synthetic",
         "config": {"workload": wl.name, "tokens": T,
                    "layers": [[L.name, L.m, L.k] for L in wl.layers], "rank": r,
