@@ -942,8 +942,9 @@ __global__ __launch_bounds__(GR_THREADS) void k_grid_w(GridArgs a) {
       // Integer Phi0 on a 4-bit grid: when |c| max_i ||A_i|| max_j ||B_j|| over all rows of the
       // block's rounds and all columns of its strip is below 1/2, every sub-tile has q = Phi0 and
       // nothing clips (the per-sub-tile test below would pass everywhere), so the block copies
-      // Phi0 without staging B fragments.  The test uses maxima of the same norm bounds.
-      if (B4 || a.bits == 4) {
+      // Phi0 without staging B fragments.  The test uses maxima of the same norm bounds and covers
+      // up to four rounds (the launcher's largest nit).
+      if ((B4 || a.bits == 4) && a.nit <= 4) {
         // column sums of squares of the wave's sub-tile, straight from the loaded values: lanes
         // l, l ^ 16, l ^ 32, l ^ 48 hold the 32 ranks of the same 4 columns
         float cs[4] = {0.f, 0.f, 0.f, 0.f}, m = 0.f;
